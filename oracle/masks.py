@@ -1,0 +1,135 @@
+"""Brute-force mask enumeration (oracle; test infrastructure only).
+
+A mask M over an L x L attention matrix has M[i, j] = 1 when query row i
+attends to key column j (section 4.1 maps M[i][j] to the point (j, i), so the
+x coordinate is the column and y the row).  Each pattern is its defining
+predicate, evaluated at every (i, j) -- O(L^2), no structure exploited.
+
+The predicates restate the workload descriptions:
+
+* window        |i - j| <= w
+* blocked       j lies in the block of i or in the block before it (block 0
+                has no predecessor)
+* strided_local causal: j in [i - local + 1, i], or (j mod stride == stride - 1
+                and j <= i); a column that satisfies both counts once
+* dilated       j - i is a multiple of the dilation g and |j - i| <= g * w
+* window_global |i - j| <= w, or i < G (global rows), or j < G (global columns)
+* full          every (i, j)
+"""
+from __future__ import annotations
+
+from typing import Callable, Dict, List
+
+import numpy as np
+
+
+def predicate(kind: str, params: Dict[str, int]) -> Callable[[int, int], bool]:
+    """Scalar predicate M(i, j) -> bool for a pattern."""
+    p = dict(params)
+    if kind == "window":
+        w = p["w"]
+        return lambda i, j: abs(i - j) <= w
+    if kind == "blocked":
+        b = p["block"]
+        return lambda i, j: (j // b) == (i // b) or (j // b) == (i // b) - 1
+    if kind == "strided_local":
+        n, s = p["local"], p["stride"]
+        return lambda i, j: (i - n < j <= i) or (j % s == s - 1 and j <= i)
+    if kind == "dilated":
+        w, g = p["w"], p["dilation"]
+        return lambda i, j: (j - i) % g == 0 and abs(j - i) <= g * w
+    if kind == "window_global":
+        w, G = p["w"], p["n_global"]
+        return lambda i, j: abs(i - j) <= w or i < G or j < G
+    if kind == "full":
+        return lambda i, j: True
+    raise ValueError(f"unknown pattern kind {kind!r}")
+
+
+def dense_mask(kind: str, params: Dict[str, int], L: int) -> np.ndarray:
+    """Boolean [L, L] mask, the predicate evaluated on the full (i, j) grid."""
+    p = dict(params)
+    i = np.arange(L, dtype=np.int64)[:, None]
+    j = np.arange(L, dtype=np.int64)[None, :]
+    if kind == "window":
+        m = np.abs(i - j) <= p["w"]
+    elif kind == "blocked":
+        b = p["block"]
+        m = ((j // b) == (i // b)) | ((j // b) == (i // b) - 1)
+    elif kind == "strided_local":
+        n, s = p["local"], p["stride"]
+        m = ((j > i - n) & (j <= i)) | ((j % s == s - 1) & (j <= i))
+    elif kind == "dilated":
+        w, g = p["w"], p["dilation"]
+        m = ((j - i) % g == 0) & (np.abs(j - i) <= g * w)
+    elif kind == "window_global":
+        w, G = p["w"], p["n_global"]
+        m = (np.abs(i - j) <= w) | (i < G) | (j < G)
+    elif kind == "full":
+        m = np.ones((L, L), dtype=bool)
+    else:
+        raise ValueError(f"unknown pattern kind {kind!r}")
+    return np.array(np.broadcast_to(m, (L, L)), dtype=bool, copy=True)
+
+
+def dense_mask_loops(kind: str, params: Dict[str, int], L: int) -> np.ndarray:
+    """Same mask from the scalar predicate with plain Python loops (small L)."""
+    f = predicate(kind, params)
+    m = np.zeros((L, L), dtype=bool)
+    for i in range(L):
+        for j in range(L):
+            m[i, j] = f(i, j)
+    return m
+
+
+def csr(mask: np.ndarray):
+    """(row_ptr int64[L+1], col_idx int64[nnz]) of a boolean mask.
+
+    Columns are listed in ascending order within each row: the order the
+    row-compressed row-major ACSR layout stores a row's values in (section 5.1).
+    """
+    mask = np.asarray(mask, dtype=bool)
+    counts = mask.sum(axis=1).astype(np.int64)
+    row_ptr = np.zeros(mask.shape[0] + 1, dtype=np.int64)
+    np.cumsum(counts, out=row_ptr[1:])
+    col_idx = np.nonzero(mask)[1].astype(np.int64)   # row-major traversal
+    return row_ptr, col_idx
+
+
+def row_columns(kind: str, params: Dict[str, int], L: int, i: int) -> np.ndarray:
+    """Ascending key columns of one row, by brute force over every j."""
+    f = predicate(kind, params)
+    return np.array([j for j in range(L) if f(i, j)], dtype=np.int64)
+
+
+def row_columns_fast(kind: str, params: Dict[str, int], L: int, rows) -> List[np.ndarray]:
+    """Ascending columns of several rows, the predicate vectorised over j."""
+    out = []
+    j = np.arange(L, dtype=np.int64)
+    for i in rows:
+        m = dense_mask_row(kind, params, L, int(i), j)
+        out.append(np.nonzero(m)[0].astype(np.int64))
+    return out
+
+
+def dense_mask_row(kind, params, L, i, j=None) -> np.ndarray:
+    p = dict(params)
+    if j is None:
+        j = np.arange(L, dtype=np.int64)
+    if kind == "window":
+        return np.abs(i - j) <= p["w"]
+    if kind == "blocked":
+        b = p["block"]
+        return ((j // b) == (i // b)) | ((j // b) == (i // b) - 1)
+    if kind == "strided_local":
+        n, s = p["local"], p["stride"]
+        return ((j > i - n) & (j <= i)) | ((j % s == s - 1) & (j <= i))
+    if kind == "dilated":
+        w, g = p["w"], p["dilation"]
+        return ((j - i) % g == 0) & (np.abs(j - i) <= g * w)
+    if kind == "window_global":
+        w, G = p["w"], p["n_global"]
+        return (np.abs(i - j) <= w) | (i < G) | (j < G)
+    if kind == "full":
+        return np.ones(L, dtype=bool)
+    raise ValueError(f"unknown pattern kind {kind!r}")
