@@ -1,0 +1,371 @@
+"""Sparse multi-head self-attention over ACSR masks on MI355X (gfx950).
+
+Thin Python binding of ``libsplat.so`` (C ABI in ``include/splat.h``): this
+module only marshals arguments -- PyTorch supplies device memory and the
+stream, every step of the computation runs in the library's HIP kernels.
+There is no fallback: if the library is not built, ``load()`` raises.
+
+    import paper_2407_16847_amd as splat
+    pat = splat.Pattern.window_global(4096, w=512, n_global=64)
+    acsr = splat.Acsr(pat)                       # host analysis + device upload
+    O = splat.sparse_mhsa_fwd(acsr, Q, K, V, scale)   # fused forward
+    S = splat.rsddmm(acsr, Q, K, scale)          # unfused: SDDMM
+    P = splat.row_softmax(acsr, S)               #          softmax over non-zeros
+    O = splat.rspmm(acsr, P, V)                  #          SpMM
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import numpy as np
+import torch  # loaded first: libsplat then binds to the HIP runtime torch uses
+
+__all__ = [
+    "SplatError", "Pattern", "Acsr", "load", "lib_path", "rsddmm", "row_softmax", "rspmm",
+    "sparse_mhsa_fwd", "MAX_RUNS", "MAX_TERMS",
+]
+
+MAX_TERMS = 8
+MAX_RUNS = 4
+F32, BF16 = 0, 1
+_STATUS = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "NOT_REGULAR", 4: "OOM", 5: "HIP",
+           6: "NO_DEVICE"}
+
+
+class SplatError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"SPLAT_ERR_{_STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = _STATUS.get(status, str(status))
+
+
+class AffineTerm(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("row_lo", "row_hi", "group", "lo_i", "lo_q", "lo_c", "hi_i", "hi_q", "hi_c", "stride")]
+
+
+class PatternDesc(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("n_terms", ctypes.c_int32), ("terms", AffineTerm * MAX_TERMS)]
+
+
+class AcsrInfo(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("max_row_nnz", ctypes.c_int32), ("max_runs", ctypes.c_int32),
+                ("on_device", ctypes.c_int32), ("device", ctypes.c_int32), ("bm", ctypes.c_int32),
+                ("bn", ctypes.c_int32), ("n_groups", ctypes.c_int32), ("n_tiles", ctypes.c_int32),
+                ("n_full_tiles", ctypes.c_int32), ("nnz", ctypes.c_int64), ("computed", ctypes.c_int64)]
+
+
+_LIB: Optional[ctypes.CDLL] = None
+
+
+def lib_path() -> str:
+    return os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsplat.so")
+
+
+def load() -> ctypes.CDLL:
+    """Load libsplat.so (built in-tree).  Raises if it is missing."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = lib_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -m paper_2407_16847_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(path)
+    i32, i64, vp, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
+    P = ctypes.POINTER
+    sig = {
+        "splat_pattern_window": [i32, i32, P(PatternDesc)],
+        "splat_pattern_blocked": [i32, i32, P(PatternDesc)],
+        "splat_pattern_strided_local": [i32, i32, i32, P(PatternDesc)],
+        "splat_pattern_dilated": [i32, i32, i32, P(PatternDesc)],
+        "splat_pattern_window_global": [i32, i32, i32, P(PatternDesc)],
+        "splat_pattern_full": [i32, P(PatternDesc)],
+        "splat_acsr_build": [P(PatternDesc), P(vp)],
+        "splat_acsr_from_mask": [i32, vp, P(vp)],
+        "splat_acsr_info": [vp, P(AcsrInfo)],
+        "splat_acsr_export": [vp, vp, vp],
+        "splat_acsr_row_runs": [vp, i32, vp, P(i32)],
+        "splat_acsr_export_plan": [vp, vp, vp, vp],
+        "splat_acsr_tile_row_mask": [vp, i32, i32, P(ctypes.c_uint64)],
+        "splat_rsddmm": [vp, i32, i32, i32, i32, vp, vp, f32, vp, vp],
+        "splat_row_softmax": [vp, i32, i32, vp, vp, vp],
+        "splat_rspmm": [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp],
+        "splat_sparse_mhsa_fwd": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, i32, vp],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.splat_acsr_destroy.argtypes = [vp]
+    lib.splat_acsr_destroy.restype = None
+    lib.splat_last_error.restype = ctypes.c_char_p
+    lib.splat_version.restype = ctypes.c_char_p
+    _LIB = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        msg = load().splat_last_error().decode(errors="replace")
+        raise SplatError(status, msg)
+
+
+# ---------------------------------------------------------------------------
+class Pattern:
+    """A pattern descriptor (union of affine terms, see include/splat.h)."""
+
+    def __init__(self, desc: PatternDesc):
+        self.desc = desc
+
+    @property
+    def L(self) -> int:
+        return int(self.desc.L)
+
+    @classmethod
+    def _make(cls, fn: str, *args) -> "Pattern":
+        d = PatternDesc()
+        _check(getattr(load(), fn)(*args, ctypes.byref(d)))
+        return cls(d)
+
+    @classmethod
+    def window(cls, L, w):
+        return cls._make("splat_pattern_window", L, w)
+
+    @classmethod
+    def blocked(cls, L, block):
+        return cls._make("splat_pattern_blocked", L, block)
+
+    @classmethod
+    def strided_local(cls, L, local, stride):
+        return cls._make("splat_pattern_strided_local", L, local, stride)
+
+    @classmethod
+    def dilated(cls, L, w, dilation):
+        return cls._make("splat_pattern_dilated", L, w, dilation)
+
+    @classmethod
+    def window_global(cls, L, w, n_global):
+        return cls._make("splat_pattern_window_global", L, w, n_global)
+
+    @classmethod
+    def full(cls, L):
+        return cls._make("splat_pattern_full", L)
+
+    @classmethod
+    def from_terms(cls, L: int, terms) -> "Pattern":
+        """terms: iterable of dicts with the AffineTerm field names (defaults:
+        rows [0, L), group 1, stride 1, coefficients 0)."""
+        d = PatternDesc()
+        d.L = L
+        terms = list(terms)
+        if len(terms) > MAX_TERMS:
+            raise ValueError(f"at most {MAX_TERMS} terms")
+        d.n_terms = len(terms)
+        for k, t in enumerate(terms):
+            base = dict(row_lo=0, row_hi=L, group=1, lo_i=0, lo_q=0, lo_c=0, hi_i=0, hi_q=0, hi_c=0,
+                        stride=1)
+            base.update(t)
+            for f, v in base.items():
+                setattr(d.terms[k], f, int(v))
+        return cls(d)
+
+    @classmethod
+    def named(cls, kind: str, params: dict, L: int) -> "Pattern":
+        """A workload pattern by kind name and parameters."""
+        p = dict(params)
+        if kind == "window":
+            return cls.window(L, p["w"])
+        if kind == "blocked":
+            return cls.blocked(L, p["block"])
+        if kind == "strided_local":
+            return cls.strided_local(L, p["local"], p["stride"])
+        if kind == "dilated":
+            return cls.dilated(L, p["w"], p["dilation"])
+        if kind == "window_global":
+            return cls.window_global(L, p["w"], p["n_global"])
+        if kind == "full":
+            return cls.full(L)
+        raise ValueError(f"unknown pattern kind {kind!r}")
+
+
+class Acsr:
+    """An ACSR handle: per-row affine runs + work plan, on the current device."""
+
+    def __init__(self, pattern: Optional[Pattern] = None, *, mask: Optional[np.ndarray] = None):
+        lib = load()
+        h = ctypes.c_void_p()
+        if mask is not None:
+            m = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
+            if m.ndim != 2 or m.shape[0] != m.shape[1]:
+                raise ValueError("mask must be a square [L, L] array")
+            _check(lib.splat_acsr_from_mask(int(m.shape[0]), m.ctypes.data_as(ctypes.c_void_p),
+                                            ctypes.byref(h)))
+        else:
+            if pattern is None:
+                raise ValueError("need a pattern or a mask")
+            _check(lib.splat_acsr_build(ctypes.byref(pattern.desc), ctypes.byref(h)))
+        self._h = h
+        self._lib = lib
+        self._info = self.info()
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self._lib.splat_acsr_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if not self._h.value:
+            raise ValueError("ACSR handle is closed")
+        return self._h
+
+    def info(self) -> dict:
+        inf = AcsrInfo()
+        _check(self._lib.splat_acsr_info(self.handle, ctypes.byref(inf)))
+        return {f: getattr(inf, f) for f, _ in AcsrInfo._fields_}
+
+    @property
+    def L(self) -> int:
+        return int(self._info["L"])
+
+    @property
+    def nnz(self) -> int:
+        return int(self._info["nnz"])
+
+    def export(self) -> Tuple[np.ndarray, np.ndarray]:
+        rp = np.zeros(self.L + 1, dtype=np.int32)
+        ci = np.zeros(max(self.nnz, 1), dtype=np.int32)
+        _check(self._lib.splat_acsr_export(self.handle, rp.ctypes.data_as(ctypes.c_void_p),
+                                           ci.ctypes.data_as(ctypes.c_void_p)))
+        return rp, ci[: self.nnz]
+
+    def row_runs(self, row: int):
+        buf = np.zeros(3 * MAX_RUNS, dtype=np.int32)
+        n = ctypes.c_int32()
+        _check(self._lib.splat_acsr_row_runs(self.handle, int(row), buf.ctypes.data_as(ctypes.c_void_p),
+                                             ctypes.byref(n)))
+        return [tuple(int(x) for x in buf[3 * r:3 * r + 3]) for r in range(n.value)]
+
+    def export_plan(self):
+        inf = self.info()
+        g = np.zeros((inf["n_groups"], 4), dtype=np.int32)
+        rows = np.zeros(self.L, dtype=np.int32)
+        t = np.zeros((max(inf["n_tiles"], 1), 4), dtype=np.int32)
+        _check(self._lib.splat_acsr_export_plan(self.handle, g.ctypes.data_as(ctypes.c_void_p),
+                                                rows.ctypes.data_as(ctypes.c_void_p),
+                                                t.ctypes.data_as(ctypes.c_void_p)))
+        return g, rows, t[: inf["n_tiles"]]
+
+    def tile_row_mask(self, tile: int, row: int) -> int:
+        b = ctypes.c_uint64()
+        _check(self._lib.splat_acsr_tile_row_mask(self.handle, int(tile), int(row), ctypes.byref(b)))
+        return int(b.value)
+
+
+# ---------------------------------------------------------------------------
+_DT = {torch.float32: F32, torch.bfloat16: BF16}
+
+
+def _dense(x: torch.Tensor, name: str, acsr: Acsr, d: Optional[int] = None):
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if x.dtype not in _DT:
+        raise TypeError(f"{name} must be float32 or bfloat16, got {x.dtype}")
+    if x.dim() != 4 or x.shape[2] != acsr.L:
+        raise ValueError(f"{name} must be [B, H, L={acsr.L}, d], got {tuple(x.shape)}")
+    if d is not None and x.shape[3] != d:
+        raise ValueError(f"{name} has d={x.shape[3]}, expected {d}")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return x
+
+
+def _stream() -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _out_dtype(dtype: Optional[torch.dtype], default: torch.dtype) -> torch.dtype:
+    dt = default if dtype is None else dtype
+    if dt not in _DT:
+        raise TypeError("out_dtype must be float32 or bfloat16")
+    return dt
+
+
+def rsddmm(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, scale: float,
+           S: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """S[b,h,:] = scale * (Q K^T) sampled at the mask, ACSR (CSR) order, fp32."""
+    _dense(Q, "Q", acsr)
+    B, H, L, d = Q.shape
+    _dense(K, "K", acsr, d)
+    if K.dtype != Q.dtype or K.shape[:2] != Q.shape[:2]:
+        raise ValueError("K must match Q in dtype, B and H")
+    if S is None:
+        S = torch.empty((B, H, acsr.nnz), dtype=torch.float32, device=Q.device)
+    elif S.dtype != torch.float32 or tuple(S.shape) != (B, H, acsr.nnz) or not S.is_contiguous():
+        raise ValueError(f"S must be a contiguous float32 [B, H, {acsr.nnz}] tensor")
+    _check(load().splat_rsddmm(acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(),
+                               float(scale), S.data_ptr() if S.numel() else None, _stream()))
+    return S
+
+
+def row_softmax(acsr: Acsr, S: torch.Tensor, P: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Softmax over each row's non-zeros; P may be S (in place)."""
+    if S.dtype != torch.float32 or S.dim() != 3 or S.shape[2] != acsr.nnz or not S.is_contiguous():
+        raise ValueError(f"S must be a contiguous float32 [B, H, {acsr.nnz}] tensor")
+    if not S.is_cuda:
+        raise TypeError("S must be a CUDA (HIP) tensor")
+    B, H, _ = S.shape
+    if P is None:
+        P = torch.empty_like(S)
+    elif P.dtype != torch.float32 or P.shape != S.shape or not P.is_contiguous():
+        raise ValueError("P must be a contiguous float32 tensor shaped like S")
+    _check(load().splat_row_softmax(acsr.handle, B, H, S.data_ptr() if S.numel() else None,
+                                    P.data_ptr() if P.numel() else None, _stream()))
+    return P
+
+
+def rspmm(acsr: Acsr, P: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor] = None,
+          out_dtype: Optional[torch.dtype] = None) -> torch.Tensor:
+    """O = P V with P in ACSR (CSR) order."""
+    _dense(V, "V", acsr)
+    B, H, L, d = V.shape
+    if P.dtype != torch.float32 or tuple(P.shape) != (B, H, acsr.nnz) or not P.is_contiguous():
+        raise ValueError(f"P must be a contiguous float32 [B, H, {acsr.nnz}] tensor")
+    odt = _out_dtype(out_dtype if O is None else O.dtype, V.dtype)
+    if O is None:
+        O = torch.empty((B, H, L, d), dtype=odt, device=V.device)
+    else:
+        _dense(O, "O", acsr, d)
+    _check(load().splat_rspmm(acsr.handle, _DT[V.dtype], B, H, d, P.data_ptr() if P.numel() else None,
+                              V.data_ptr(), O.data_ptr(), _DT[O.dtype], _stream()))
+    return O
+
+
+def sparse_mhsa_fwd(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: float,
+                    O: Optional[torch.Tensor] = None,
+                    out_dtype: Optional[torch.dtype] = None) -> torch.Tensor:
+    """Fused O = softmax_nz(scale * M (x) Q K^T) V."""
+    _dense(Q, "Q", acsr)
+    B, H, L, d = Q.shape
+    for n, x in (("K", K), ("V", V)):
+        _dense(x, n, acsr, d)
+        if x.dtype != Q.dtype or x.shape[:2] != Q.shape[:2]:
+            raise ValueError(f"{n} must match Q in dtype, B and H")
+    odt = _out_dtype(out_dtype if O is None else O.dtype, Q.dtype)
+    if O is None:
+        O = torch.empty((B, H, L, d), dtype=odt, device=Q.device)
+    else:
+        _dense(O, "O", acsr, d)
+    _check(load().splat_sparse_mhsa_fwd(acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(),
+                                        V.data_ptr(), float(scale), O.data_ptr(), _DT[O.dtype],
+                                        _stream()))
+    return O

@@ -1,0 +1,359 @@
+// api.hip -- the C ABI declared in include/splat.h: argument validation,
+// ACSR handle lifetime (host analysis + one device upload) and kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/splat.h"
+#include "acsr_host.hpp"
+#include "launch.hpp"
+
+using splat::DevAcsr;
+using splat::HostAcsr;
+
+struct splat_acsr {
+  HostAcsr host;
+  int device = -1;
+  void* dmem = nullptr;
+  DevAcsr dev{};
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+splat_status fail(splat_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+splat_status ok() { return SPLAT_OK; }
+
+// One allocation holds every metadata array, each 256-byte aligned.
+splat_status upload(splat_acsr* h) {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n == 0) {
+    (void)hipGetLastError();  // a missing GPU is not an error for a host-only handle
+    h->device = -1;
+    return SPLAT_OK;
+  }
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPLAT_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  const HostAcsr& a = h->host;
+  auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t s_rowptr = al(sizeof(int32_t) * (a.L + 1));
+  const size_t s_runs = al(sizeof(splat::RowRuns) * a.L);
+  const size_t s_rows = al(sizeof(int32_t) * a.L);
+  const size_t s_groups = al(sizeof(splat::Group) * a.groups.size());
+  const size_t s_tiles = al(sizeof(splat::Tile) * (a.tiles.size() + 1));
+  const size_t total = s_rowptr + s_runs + s_rows + s_groups + s_tiles;
+  void* mem = nullptr;
+  e = hipMalloc(&mem, total);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SPLAT_ERR_OOM, "hipMalloc(%zu) for ACSR metadata: %s", total, hipGetErrorString(e));
+  }
+  char* p = (char*)mem;
+  struct Part {
+    const void* src;
+    size_t n, sz;
+  } parts[] = {{a.row_ptr.data(), sizeof(int32_t) * (a.L + 1), s_rowptr},
+               {a.runs.data(), sizeof(splat::RowRuns) * a.L, s_runs},
+               {a.rows.data(), sizeof(int32_t) * a.L, s_rows},
+               {a.groups.data(), sizeof(splat::Group) * a.groups.size(), s_groups},
+               {a.tiles.data(), sizeof(splat::Tile) * a.tiles.size(), s_tiles}};
+  char* dst[5];
+  for (int k = 0; k < 5; ++k) {
+    dst[k] = p;
+    if (parts[k].n) {
+      e = hipMemcpy(p, parts[k].src, parts[k].n, hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        (void)hipFree(mem);
+        return fail(SPLAT_ERR_HIP, "hipMemcpy of ACSR metadata: %s", hipGetErrorString(e));
+      }
+    }
+    p += parts[k].sz;
+  }
+  h->dmem = mem;
+  h->device = dev;
+  h->dev.L = a.L;
+  h->dev.nnz = a.nnz;
+  h->dev.n_groups = (int32_t)a.groups.size();
+  h->dev.row_ptr = (const int32_t*)dst[0];
+  h->dev.runs = (const splat::RowRuns*)dst[1];
+  h->dev.rows = (const int32_t*)dst[2];
+  h->dev.groups = (const splat::Group*)dst[3];
+  h->dev.tiles = (const splat::Tile*)dst[4];
+  return SPLAT_OK;
+}
+
+splat_status finish_build(splat_acsr* h, splat_status s, const std::string& err, splat_acsr_t* out) {
+  if (s != SPLAT_OK) {
+    delete h;
+    return fail(s, "%s", err.c_str());
+  }
+  s = upload(h);
+  if (s != SPLAT_OK) {
+    delete h;
+    return s;
+  }
+  *out = h;
+  return ok();
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Validation shared by the compute calls.  Returns SPLAT_OK or the failure.
+splat_status check_handle(splat_acsr_t h, int32_t B, int32_t H) {
+  if (!h) return fail(SPLAT_ERR_INVALID_ARG, "ACSR handle is NULL");
+  if (B < 1 || H < 1 || (int64_t)B * H > 65535)
+    return fail(SPLAT_ERR_INVALID_ARG, "B and H must be >= 1 with B*H <= 65535 (got B=%d, H=%d)", B, H);
+  if (h->device < 0)
+    return fail(SPLAT_ERR_NO_DEVICE, "the ACSR handle was built without a GPU");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPLAT_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev != h->device)
+    return fail(SPLAT_ERR_INVALID_ARG, "current device %d differs from the handle's device %d", dev,
+                h->device);
+  return SPLAT_OK;
+}
+
+splat_status check_d(int32_t d) {
+  if (d != 64 && d != 128) return fail(SPLAT_ERR_UNSUPPORTED, "d must be 64 or 128, got %d", d);
+  return SPLAT_OK;
+}
+
+splat_status check_dtype(splat_dtype t, const char* what) {
+  if (t != SPLAT_F32 && t != SPLAT_BF16)
+    return fail(SPLAT_ERR_INVALID_ARG, "%s must be SPLAT_F32 or SPLAT_BF16", what);
+  return SPLAT_OK;
+}
+
+splat_status check_ptr(const void* p, const char* what) {
+  if (!p) return fail(SPLAT_ERR_INVALID_ARG, "%s is NULL", what);
+  if (!aligned16(p)) return fail(SPLAT_ERR_INVALID_ARG, "%s is not 16-byte aligned", what);
+  return SPLAT_OK;
+}
+
+splat_status launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(SPLAT_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+#define CHECK(x)                     \
+  do {                               \
+    splat_status _s = (x);           \
+    if (_s != SPLAT_OK) return _s;   \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* splat_last_error(void) { return g_err.c_str(); }
+
+const char* splat_version(void) { return "splat-mi355x 0.1 (gfx950)"; }
+
+splat_status splat_pattern_window(int32_t L, int32_t w, splat_pattern_desc* out) {
+  return splat::pattern_window(L, w, out) == SPLAT_OK ? ok() : fail(SPLAT_ERR_INVALID_ARG, "bad window pattern arguments");
+}
+splat_status splat_pattern_blocked(int32_t L, int32_t block, splat_pattern_desc* out) {
+  return splat::pattern_blocked(L, block, out) == SPLAT_OK ? ok() : fail(SPLAT_ERR_INVALID_ARG, "bad blocked pattern arguments");
+}
+splat_status splat_pattern_strided_local(int32_t L, int32_t local, int32_t stride, splat_pattern_desc* out) {
+  return splat::pattern_strided_local(L, local, stride, out) == SPLAT_OK ? ok() : fail(SPLAT_ERR_INVALID_ARG, "bad strided_local pattern arguments");
+}
+splat_status splat_pattern_dilated(int32_t L, int32_t w, int32_t dilation, splat_pattern_desc* out) {
+  return splat::pattern_dilated(L, w, dilation, out) == SPLAT_OK ? ok() : fail(SPLAT_ERR_INVALID_ARG, "bad dilated pattern arguments");
+}
+splat_status splat_pattern_window_global(int32_t L, int32_t w, int32_t n_global, splat_pattern_desc* out) {
+  return splat::pattern_window_global(L, w, n_global, out) == SPLAT_OK ? ok() : fail(SPLAT_ERR_INVALID_ARG, "bad window_global pattern arguments");
+}
+splat_status splat_pattern_full(int32_t L, splat_pattern_desc* out) {
+  return splat::pattern_full(L, out) == SPLAT_OK ? ok() : fail(SPLAT_ERR_INVALID_ARG, "bad full pattern arguments");
+}
+
+splat_status splat_acsr_build(const splat_pattern_desc* desc, splat_acsr_t* out) {
+  if (!desc || !out) return fail(SPLAT_ERR_INVALID_ARG, "desc and out must be non-NULL");
+  splat_acsr* h = new (std::nothrow) splat_acsr();
+  if (!h) return fail(SPLAT_ERR_OOM, "host allocation failed");
+  std::string err;
+  splat_status s;
+  try {
+    s = splat::build_from_desc(*desc, h->host, err);
+  } catch (const std::bad_alloc&) {
+    s = SPLAT_ERR_OOM;
+    err = "host allocation failed during the analysis";
+  }
+  return finish_build(h, s, err, out);
+}
+
+splat_status splat_acsr_from_mask(int32_t L, const uint8_t* mask, splat_acsr_t* out) {
+  if (!out) return fail(SPLAT_ERR_INVALID_ARG, "out must be non-NULL");
+  splat_acsr* h = new (std::nothrow) splat_acsr();
+  if (!h) return fail(SPLAT_ERR_OOM, "host allocation failed");
+  std::string err;
+  splat_status s;
+  try {
+    s = splat::build_from_mask(L, mask, h->host, err);
+  } catch (const std::bad_alloc&) {
+    s = SPLAT_ERR_OOM;
+    err = "host allocation failed during the analysis";
+  }
+  return finish_build(h, s, err, out);
+}
+
+void splat_acsr_destroy(splat_acsr_t h) {
+  if (!h) return;
+  if (h->dmem) (void)hipFree(h->dmem);
+  delete h;
+}
+
+splat_status splat_acsr_info(splat_acsr_t h, splat_acsr_info_t* out) {
+  if (!h || !out) return fail(SPLAT_ERR_INVALID_ARG, "handle and out must be non-NULL");
+  const HostAcsr& a = h->host;
+  std::memset(out, 0, sizeof(*out));
+  out->L = a.L;
+  out->max_row_nnz = a.max_row_nnz;
+  out->max_runs = a.max_runs;
+  out->on_device = h->device >= 0;
+  out->device = h->device;
+  out->bm = splat::kBM;
+  out->bn = splat::kBN;
+  out->n_groups = (int32_t)a.groups.size();
+  out->n_tiles = (int32_t)a.tiles.size();
+  out->n_full_tiles = a.n_full;
+  out->nnz = a.nnz;
+  out->computed = a.computed;
+  return ok();
+}
+
+splat_status splat_acsr_export(splat_acsr_t h, int32_t* row_ptr, int32_t* col_idx) {
+  if (!h || !row_ptr || (!col_idx && h->host.nnz > 0))
+    return fail(SPLAT_ERR_INVALID_ARG, "handle, row_ptr and col_idx must be non-NULL");
+  const HostAcsr& a = h->host;
+  std::memcpy(row_ptr, a.row_ptr.data(), sizeof(int32_t) * (a.L + 1));
+  for (int32_t i = 0; i < a.L; ++i) {
+    int32_t* o = col_idx + a.row_ptr[i];
+    for (int r = 0; r < SPLAT_MAX_RUNS; ++r) {
+      const splat::Run& q = a.runs[i].r[r];
+      for (int32_t k = 0; k < q.count; ++k) o[q.prefix + k] = q.start + q.stride * k;
+    }
+  }
+  return ok();
+}
+
+splat_status splat_acsr_row_runs(splat_acsr_t h, int32_t row, int32_t* runs, int32_t* nruns) {
+  if (!h || !runs || !nruns) return fail(SPLAT_ERR_INVALID_ARG, "NULL argument");
+  if (row < 0 || row >= h->host.L) return fail(SPLAT_ERR_INVALID_ARG, "row %d out of range", row);
+  *nruns = h->host.nruns[row];
+  for (int r = 0; r < SPLAT_MAX_RUNS; ++r) {
+    const splat::Run& q = h->host.runs[row].r[r];
+    runs[3 * r] = q.start;
+    runs[3 * r + 1] = q.stride;
+    runs[3 * r + 2] = q.count;
+  }
+  return ok();
+}
+
+splat_status splat_acsr_export_plan(splat_acsr_t h, int32_t* groups, int32_t* rows, int32_t* tiles) {
+  if (!h || !groups || !rows || !tiles) return fail(SPLAT_ERR_INVALID_ARG, "NULL argument");
+  const HostAcsr& a = h->host;
+  for (size_t g = 0; g < a.groups.size(); ++g) {
+    groups[4 * g] = a.groups[g].row_off;
+    groups[4 * g + 1] = a.groups[g].nrows;
+    groups[4 * g + 2] = a.groups[g].tile_begin;
+    groups[4 * g + 3] = a.groups[g].tile_end;
+  }
+  std::memcpy(rows, a.rows.data(), sizeof(int32_t) * a.L);
+  for (size_t t = 0; t < a.tiles.size(); ++t) {
+    tiles[4 * t] = a.tiles[t].kb;
+    tiles[4 * t + 1] = a.tiles[t].ks;
+    tiles[4 * t + 2] = a.tiles[t].nk;
+    tiles[4 * t + 3] = a.tiles[t].flags;
+  }
+  return ok();
+}
+
+splat_status splat_acsr_tile_row_mask(splat_acsr_t h, int32_t tile, int32_t row, uint64_t* bits) {
+  if (!h || !bits) return fail(SPLAT_ERR_INVALID_ARG, "NULL argument");
+  if (tile < 0 || tile >= (int32_t)h->host.tiles.size())
+    return fail(SPLAT_ERR_INVALID_ARG, "tile %d out of range", tile);
+  if (row < 0 || row >= h->host.L) return fail(SPLAT_ERR_INVALID_ARG, "row %d out of range", row);
+  const splat::Tile& t = h->host.tiles[tile];
+  *bits = splat::tile_row_bits(h->host.runs[row], t.kb, t.ks, t.nk);
+  return ok();
+}
+
+splat_status splat_rsddmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                          const void* Q, const void* K, float scale, float* S, void* stream) {
+  CHECK(check_handle(h, B, H));
+  CHECK(check_dtype(dtype, "dtype"));
+  CHECK(check_d(d));
+  CHECK(check_ptr(Q, "Q"));
+  CHECK(check_ptr(K, "K"));
+  if (h->host.nnz == 0) return ok();
+  CHECK(check_ptr(S, "S"));
+  return launched(splat::launch_rsddmm_rows(h->dev, dtype, B * H, d, Q, K, scale, S,
+                                            (hipStream_t)stream),
+                  "rsddmm");
+}
+
+splat_status splat_row_softmax(splat_acsr_t h, int32_t B, int32_t H, const float* S, float* P,
+                               void* stream) {
+  CHECK(check_handle(h, B, H));
+  if (h->host.nnz == 0) return ok();
+  CHECK(check_ptr(S, "S"));
+  CHECK(check_ptr(P, "P"));
+  const size_t bytes = sizeof(float) * (size_t)B * H * h->host.nnz;
+  const char *s0 = (const char*)S, *p0 = (const char*)P;
+  if (s0 != p0 && s0 < p0 + bytes && p0 < s0 + bytes)
+    return fail(SPLAT_ERR_INVALID_ARG, "S and P overlap without being equal");
+  return launched(splat::launch_softmax_rows(h->dev, B * H, S, P, (hipStream_t)stream), "row_softmax");
+}
+
+splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                         const float* P, const void* V, void* O, splat_dtype out_dtype, void* stream) {
+  CHECK(check_handle(h, B, H));
+  CHECK(check_dtype(dtype, "dtype"));
+  CHECK(check_dtype(out_dtype, "out_dtype"));
+  CHECK(check_d(d));
+  if (h->host.nnz > 0) CHECK(check_ptr(P, "P"));
+  CHECK(check_ptr(V, "V"));
+  CHECK(check_ptr(O, "O"));
+  return launched(splat::launch_rspmm_rows(h->dev, dtype, B * H, d, P, V, O, out_dtype,
+                                           (hipStream_t)stream),
+                  "rspmm");
+}
+
+splat_status splat_sparse_mhsa_fwd(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                                   const void* Q, const void* K, const void* V, float scale,
+                                   void* O, splat_dtype out_dtype, void* stream) {
+  CHECK(check_handle(h, B, H));
+  CHECK(check_dtype(dtype, "dtype"));
+  CHECK(check_dtype(out_dtype, "out_dtype"));
+  CHECK(check_d(d));
+  CHECK(check_ptr(Q, "Q"));
+  CHECK(check_ptr(K, "K"));
+  CHECK(check_ptr(V, "V"));
+  CHECK(check_ptr(O, "O"));
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == SPLAT_BF16)
+    return launched(splat::launch_fused_mfma(h->dev, B * H, d, Q, K, V, scale, O, out_dtype, st),
+                    "sparse_mhsa_fwd");
+  return launched(splat::launch_fused_rows(h->dev, dtype, B * H, d, Q, K, V, scale, O, out_dtype, st),
+                  "sparse_mhsa_fwd");
+}
+
+}  // extern "C"

@@ -1,0 +1,40 @@
+// launch.hpp -- internal interface between the C ABI and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "acsr_core.hpp"
+
+namespace splat {
+
+// Device view of an ACSR handle's metadata.
+struct DevAcsr {
+  int32_t L;
+  int64_t nnz;
+  int32_t n_groups;
+  const int32_t* row_ptr;   // L + 1
+  const RowRuns* runs;      // L
+  const int32_t* rows;      // L (grouped)
+  const Group* groups;      // n_groups
+  const Tile* tiles;
+};
+
+// Every launcher enqueues on `st` and returns the launch status.
+// dtype / out dtype: 0 = fp32, 1 = bf16.
+
+// Row-per-wave kernels: any d in {64, 128}, both dtypes.
+hipError_t launch_rsddmm_rows(const DevAcsr& a, int dtype, int BH, int d, const void* Q,
+                              const void* K, float scale, float* S, hipStream_t st);
+hipError_t launch_softmax_rows(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st);
+hipError_t launch_rspmm_rows(const DevAcsr& a, int dtype, int BH, int d, const float* P,
+                             const void* V, void* O, int out_dtype, hipStream_t st);
+hipError_t launch_fused_rows(const DevAcsr& a, int dtype, int BH, int d, const void* Q,
+                             const void* K, const void* V, float scale, void* O, int out_dtype,
+                             hipStream_t st);
+
+// Matrix-core kernels over the tile plan: bf16 inputs, d in {64, 128}.
+hipError_t launch_fused_mfma(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
+                             const void* V, float scale, void* O, int out_dtype, hipStream_t st);
+
+}  // namespace splat

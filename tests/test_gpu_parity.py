@@ -1,0 +1,273 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Tolerances (stated by the target and derived in the comments):
+  * bf16 inputs: elementwise |O - O_ref| <= 2e-2 (O_ref is fp64 on the same
+    bf16-rounded inputs);
+  * fp32 inputs: per-row normwise max_i ||O_i - R_i||_inf / ||R_i||_inf <= 1e-5;
+  * unfused intermediates: S per-row normwise <= 1e-5 (fp32 accumulation of
+    exact bf16 products or fp32 FMA: about d * 2^-24 of ||q|| ||k||);
+    P elementwise <= 1e-5 (S error times P plus fp32 exp/divide rounding),
+    every row of P sums to 1 within 1e-5.
+Sizes: the three small workloads at full size against the dense oracle; the
+two L = 4096 workloads at full size (the launch the benchmark times) on
+sampled rows, each computed by the per-row oracle.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import attention as oa
+from oracle import masks as om
+
+pytestmark = pytest.mark.gpu
+
+BF16_ABS = 2e-2
+F32_REL = 1e-5
+S_REL = 1e-5
+P_ABS = 1e-5
+
+
+def _dev(t):
+    return t.to("cuda")
+
+
+def _rows_normwise(x, ref):
+    """max over rows of ||x_i - r_i||_inf / ||r_i||_inf, rows of the last axis."""
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    num = np.abs(x - ref).max(axis=-1)
+    den = np.abs(ref).max(axis=-1)
+    zero = den == 0
+    assert (num[zero] == 0).all(), "rows whose reference is 0 must be exactly 0"
+    return float((num[~zero] / den[~zero]).max()) if (~zero).any() else 0.0
+
+
+def check_O(O, ref, dtype, what=""):
+    O = O.float().cpu().numpy().astype(np.float64)
+    assert np.isfinite(O).all(), f"{what}: non-finite output"
+    if dtype == "bf16":
+        err = float(np.abs(O - ref).max())
+        assert err <= BF16_ABS, f"{what}: max abs error {err:.3e} > {BF16_ABS}"
+    else:
+        err = _rows_normwise(O, ref)
+        assert err <= F32_REL, f"{what}: row-normwise rel error {err:.3e} > {F32_REL}"
+    return err
+
+
+def unfused(a, splat, Q, K, V, scale, out_dtype):
+    S = splat.rsddmm(a, Q, K, scale)
+    P = splat.row_softmax(a, S)
+    O = splat.rspmm(a, P, V, out_dtype=out_dtype)
+    return S, P, O
+
+
+def check_csr_rows(S, P, Sref, Pref, row_ptr, rows, what):
+    """S, P (numpy [nnz]) and reference lists, on the given rows."""
+    for t, i in enumerate(rows):
+        seg = slice(row_ptr[i], row_ptr[i + 1])
+        if row_ptr[i + 1] == row_ptr[i]:
+            continue
+        s, p = S[seg].astype(np.float64), P[seg].astype(np.float64)
+        es = np.abs(s - Sref[t]).max() / max(np.abs(Sref[t]).max(), 1e-30)
+        ep = np.abs(p - Pref[t]).max()
+        assert es <= S_REL, f"{what} row {i}: S rel error {es:.3e}"
+        assert ep <= P_ABS, f"{what} row {i}: P abs error {ep:.3e}"
+        assert abs(p.sum() - 1.0) <= 1e-5, f"{what} row {i}: P row sum {p.sum()}"
+
+
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_small_configs_full_oracle(gpu_lib, cfg):
+    splat = gpu_lib
+    w = workloads.get(cfg)
+    print(f"[gpu] cfg{cfg} {w.name} full-size dense oracle", flush=True)
+    Q, K, V = workloads.make_qkv(w)
+    M = om.dense_mask(w.kind, w.params, w.L)
+    ref, Sref, Pref = oa.masked_attention(Q, K, V, M, w.scale, want_csr=True)
+    a = splat.Acsr(splat.Pattern.named(w.kind, w.params, w.L))
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    errs = {}
+    for odt in (torch.float32, torch.bfloat16):
+        O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=odt)
+        torch.cuda.synchronize()
+        errs[f"fused/{odt}"] = check_O(O, ref, w.dtype if odt == torch.float32 else "bf16",
+                                       f"cfg{cfg} fused out={odt}")
+    S, P, O = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    errs["unfused"] = check_O(O, ref, w.dtype, f"cfg{cfg} unfused")
+    S, P = S.cpu().numpy(), P.cpu().numpy()
+    for b in range(w.B):
+        for h in range(w.H):
+            np.testing.assert_array_less(np.abs(P[b, h] - Pref[b, h]), P_ABS)
+            err = _rows_normwise_csr(S[b, h], Sref[b, h], om.csr(M)[0])
+            assert err <= S_REL, f"S rel {err}"
+    print(f"[gpu] cfg{cfg} errors {errs}", flush=True)
+
+
+def _rows_normwise_csr(x, ref, row_ptr):
+    worst = 0.0
+    for i in range(len(row_ptr) - 1):
+        seg = slice(row_ptr[i], row_ptr[i + 1])
+        if row_ptr[i + 1] > row_ptr[i]:
+            worst = max(worst, np.abs(x[seg] - ref[seg]).max() / np.abs(ref[seg]).max())
+    return worst
+
+
+def _sample_rows(L, extra, rng, n_random=40):
+    rows = set(r for r in extra if 0 <= r < L)
+    rows.update(rng.integers(0, L, size=n_random).tolist())
+    return sorted(rows)
+
+
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_large_configs_sampled_rows(gpu_lib, cfg):
+    """Full size, the benchmark's launch (bf16 in; fp32 and bf16 out)."""
+    splat = gpu_lib
+    w = workloads.get(cfg)
+    print(f"[gpu] cfg{cfg} {w.name} full size, sampled rows", flush=True)
+    Q, K, V = workloads.make_qkv(w)
+    a = splat.Acsr(splat.Pattern.named(w.kind, w.params, w.L))
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O32 = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+    O16 = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.bfloat16)
+    S, P, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    O32, O16, Ou = O32.cpu().numpy(), O16.float().cpu().numpy(), Ou.cpu().numpy()
+    assert np.isfinite(O32).all() and np.isfinite(O16).all() and np.isfinite(Ou).all()
+    row_ptr, _ = a.export()
+    rng = np.random.default_rng(cfg)
+    edges = [0, 1, 63, 64, 65, 127, 128, 129, 255, 256, 511, 512, 513, 576, 577, 1000, 2047, 2048,
+             w.L - 513, w.L - 512, w.L - 129, w.L - 128, w.L - 2, w.L - 1]
+    q, k, v = oa.to_f64(Q), oa.to_f64(K), oa.to_f64(V)
+    heads = sorted({(0, 0), (w.B - 1, w.H - 1)} | {(int(rng.integers(w.B)), int(rng.integers(w.H)))})
+    worst = {"fused32": 0.0, "fused16": 0.0, "unfused": 0.0}
+    Sn, Pn = None, None
+    for b, h in heads:
+        rows = _sample_rows(w.L, edges, rng)
+        cols = om.row_columns_fast(w.kind, w.params, w.L, rows)
+        Sr, Pr, Or = oa.attention_rows(q[b, h], k[b, h], v[b, h], rows, cols, w.scale)
+        for name, O in (("fused32", O32), ("fused16", O16), ("unfused", Ou)):
+            err = float(np.abs(O[b, h, rows] - Or).max())
+            worst[name] = max(worst[name], err)
+            assert err <= BF16_ABS, f"cfg{cfg} {name} head {(b, h)}: {err:.3e}"
+        Sbh = S[b, h].cpu().numpy()
+        Pbh = P[b, h].cpu().numpy()
+        check_csr_rows(Sbh, Pbh, Sr, Pr, row_ptr, rows, f"cfg{cfg} head {(b, h)}")
+    print(f"[gpu] cfg{cfg} worst abs errors {worst}", flush=True)
+
+
+# --------------------------------------------------------------------------
+# edge cases: ragged sizes, d = 128, tiny L, empty rows, full and diagonal masks
+EDGE = [
+    ("window_global", {"w": 40, "n_global": 5}, 300, 64),
+    ("dilated", {"w": 100, "dilation": 3}, 1000, 128),
+    ("strided_local", {"local": 50, "stride": 37}, 777, 64),
+    ("blocked", {"block": 64}, 130, 128),
+    ("window", {"w": 3}, 5, 64),
+    ("full", {}, 1, 64),
+    ("full", {}, 200, 64),
+    ("window", {"w": 700}, 513, 128),
+]
+
+
+@pytest.mark.parametrize("kind,params,L,d", EDGE)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_edge_cases(gpu_lib, kind, params, L, d, dtype):
+    splat = gpu_lib
+    w = workloads.Workload("edge", 2, 3, L, d, dtype, workloads.make_pattern(kind, **params), 1.0, L + d)
+    print(f"[gpu] edge {kind} {params} L={L} d={d} {dtype}", flush=True)
+    Q, K, V = workloads.make_qkv(w)
+    M = om.dense_mask(kind, params, L)
+    ref, Sref, Pref = oa.masked_attention(Q, K, V, M, w.scale, want_csr=True)
+    a = splat.Acsr(splat.Pattern.named(kind, params, L))
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+    S, P, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    check_O(O, ref, dtype, "fused")
+    check_O(Ou, ref, dtype, "unfused")
+    S, P = S.cpu().numpy(), P.cpu().numpy()
+    rp = om.csr(M)[0]
+    for b in range(2):
+        for h in range(3):
+            assert _rows_normwise_csr(S[b, h], Sref[b, h], rp) <= S_REL
+            assert np.abs(P[b, h] - Pref[b, h]).max() <= P_ABS
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_diagonal_mask_returns_v_exactly(gpu_lib, dtype):
+    splat = gpu_lib
+    w = workloads.Workload("diag", 2, 2, 333, 64, dtype, workloads.make_pattern("window", w=0), 1.0, 7)
+    Q, K, V = (_dev(x) for x in workloads.make_qkv(w))
+    a = splat.Acsr(splat.Pattern.window(w.L, 0))
+    odt = torch.float32 if dtype == "f32" else torch.bfloat16
+    O = splat.sparse_mhsa_fwd(a, Q, K, V, w.scale, out_dtype=odt)
+    Ou = splat.rspmm(a, splat.row_softmax(a, splat.rsddmm(a, Q, K, w.scale)), V, out_dtype=odt)
+    torch.cuda.synchronize()
+    assert torch.equal(O, V) and torch.equal(Ou, V)
+
+
+def test_empty_rows_give_zero(gpu_lib):
+    splat = gpu_lib
+    L = 260
+    # rows [0, 100) and [200, 260) attend to a window; rows [100, 200) to nothing
+    terms = [dict(row_lo=0, row_hi=100, lo_i=1, lo_c=-5, hi_i=1, hi_c=5),
+             dict(row_lo=200, row_hi=L, lo_i=1, lo_c=-70, hi_i=1, hi_c=0)]
+    a = splat.Acsr(splat.Pattern.from_terms(L, terms))
+    M = np.zeros((L, L), dtype=bool)
+    for i in range(L):
+        if i < 100:
+            M[i, max(0, i - 5):min(L, i + 6)] = True
+        elif i >= 200:
+            M[i, i - 70:i + 1] = True
+    assert a.nnz == int(M.sum())
+    for dtype in ("f32", "bf16"):
+        w = workloads.Workload("empty", 1, 2, L, 128, dtype, workloads.make_pattern("full"), 1.0, 3)
+        Q, K, V = workloads.make_qkv(w)
+        ref = oa.masked_attention(Q, K, V, M, w.scale)
+        Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+        O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+        Ou = splat.rspmm(a, splat.row_softmax(a, splat.rsddmm(a, Qd, Kd, w.scale)), Vd,
+                         out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert (O[:, :, 100:200] == 0).all() and (Ou[:, :, 100:200] == 0).all()
+        check_O(O, ref, dtype, "fused empty rows")
+        check_O(Ou, ref, dtype, "unfused empty rows")
+
+
+def test_softmax_in_place_and_determinism(gpu_lib):
+    splat = gpu_lib
+    w = workloads.get(2)
+    Q, K, V = (_dev(x) for x in workloads.make_qkv(w))
+    a = splat.Acsr(splat.Pattern.named(w.kind, w.params, w.L))
+    S = splat.rsddmm(a, Q, K, w.scale)
+    P = splat.row_softmax(a, S)
+    S2 = S.clone()
+    P2 = splat.row_softmax(a, S2, S2)       # in place
+    O1 = splat.sparse_mhsa_fwd(a, Q, K, V, w.scale)
+    O2 = splat.sparse_mhsa_fwd(a, Q, K, V, w.scale)
+    torch.cuda.synchronize()
+    assert P2.data_ptr() == S2.data_ptr() and torch.equal(P, P2)
+    assert torch.equal(O1, O2)
+
+
+def test_argument_errors(gpu_lib):
+    splat = gpu_lib
+    a = splat.Acsr(splat.Pattern.window(128, 4))
+    x = torch.zeros((1, 1, 128, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError):
+        splat.sparse_mhsa_fwd(a, torch.zeros((1, 1, 64, 64), dtype=torch.bfloat16, device="cuda"), x, x, 0.1)
+    with pytest.raises(splat.SplatError) as e:
+        splat.sparse_mhsa_fwd(a, torch.zeros((1, 1, 128, 32), dtype=torch.bfloat16, device="cuda"),
+                              torch.zeros((1, 1, 128, 32), dtype=torch.bfloat16, device="cuda"),
+                              torch.zeros((1, 1, 128, 32), dtype=torch.bfloat16, device="cuda"), 0.1)
+    assert e.value.name == "UNSUPPORTED"
+    lib = splat.load()
+    rc = lib.splat_sparse_mhsa_fwd(a.handle, 1, 1, 1, 64, x.data_ptr() + 2, x.data_ptr(), x.data_ptr(),
+                                   0.1, x.data_ptr(), 1, None)
+    assert rc == 1 and b"aligned" in lib.splat_last_error()
+    info = a.info()
+    assert info["on_device"] == 1 and info["device"] == torch.cuda.current_device()
