@@ -158,7 +158,7 @@ typedef struct {
   int32_t n_tiles;
   int32_t n_full_tiles;
   int64_t nnz;             /* non-zeros per (batch, head) */
-  int64_t computed;        /* rows x keys the planned tiles cover (>= nnz) */
+  int64_t computed;        /* rows x keys of the 32-row x 64-key tiles the kernels compute (>= nnz) */
 } splat_acsr_info_t;
 
 splat_status splat_acsr_info(splat_acsr_t h, splat_acsr_info_t* out);
@@ -172,9 +172,13 @@ splat_status splat_acsr_row_runs(splat_acsr_t h, int32_t row, int32_t* runs, int
 /*
  * Host copy of the work plan.  groups[4*g + {0,1,2,3}] = (first index into
  * rows, number of rows, first tile, one past the last tile), in launch order;
- * rows[L] lists every row once (grouped); tiles[4*t + {0,1,2,3}] =
- * (first key, key step, number of keys, flags) with flags bit 0 = FULL.  The
- * keys of a tile are first + step * u for u < number of keys.
+ * rows[L] lists every row once (grouped); tiles[5*t + {0,1,2,3,4}] =
+ * (first key, key step, number of keys, flags, mask block).  The keys of a
+ * tile are first + step * u for u < number of keys.  flags bit 0 = every key
+ * is in every row of the group; bits 8+2w..9+2w = the tile's state for the
+ * group's rows [32w, 32w+32): 0 none of them has a key here, 1 some do (the
+ * per-row masks are precomputed, mask block >= 0), 3 all keys in all rows.
+ * Sizes come from splat_acsr_info (n_groups, n_tiles).
  */
 splat_status splat_acsr_export_plan(splat_acsr_t h, int32_t* groups, int32_t* rows, int32_t* tiles);
 

@@ -259,7 +259,7 @@ class Acsr:
         inf = self.info()
         g = np.zeros((inf["n_groups"], 4), dtype=np.int32)
         rows = np.zeros(self.L, dtype=np.int32)
-        t = np.zeros((max(inf["n_tiles"], 1), 4), dtype=np.int32)
+        t = np.zeros((max(inf["n_tiles"], 1), 5), dtype=np.int32)
         _check(self._lib.splat_acsr_export_plan(self.handle, g.ctypes.data_as(ctypes.c_void_p),
                                                 rows.ctypes.data_as(ctypes.c_void_p),
                                                 t.ctypes.data_as(ctypes.c_void_p)))

@@ -32,7 +32,18 @@ namespace splat {
 
 constexpr int kBM = 128;   // rows per group (4 waves x 32 rows)
 constexpr int kBN = 64;    // keys per tile
+constexpr int kWaveRows = 32;  // rows of a group handled by one wavefront
+constexpr int kWavesPerGroup = kBM / kWaveRows;
+
+// Tile::flags: bit 0 = every key of the tile is in every row of the group;
+// bits 8 + 2w, 9 + 2w = state of the tile for rows [32w, 32w + 32) of the
+// group: kWaveEmpty (no row has a key here), kWavePartial (per-row masks in
+// the plan's mask block), kWaveFull (every key in every row).
 constexpr int kTileFull = 1;
+constexpr int kWaveEmpty = 0;
+constexpr int kWavePartial = 1;
+constexpr int kWaveFull = 3;
+constexpr int kWaveShift = 8;
 
 struct Run {
   int32_t start, stride, count, prefix;
@@ -48,6 +59,8 @@ struct Group {
 
 struct Tile {
   int32_t kb, ks, nk, flags;
+  int32_t mask_block;   // -1, or index of the tile's kBM per-row masks in the mask array
+  int32_t pad[3];
 };
 
 SPLAT_HD int32_t floor_div(int32_t a, int32_t b) {  // b > 0

@@ -243,6 +243,7 @@ void plan_work(HostAcsr& a) {
   a.tiles.clear();
   a.computed = 0;
   a.n_full = 0;
+  a.masks.clear();
   struct Pending {
     Group g;
     std::vector<Tile> t;
@@ -294,19 +295,39 @@ void plan_work(HostAcsr& a) {
             ++k2;
           }
         }
-        Tile t;
+        Tile t{};
         if (k2 > k1) {
-          t = Tile{c, step, k2, 0};
+          t.kb = c, t.ks = step, t.nk = k2;
           pos = last + 1;
         } else {
-          t = Tile{c, 1, dense_end - c + 1, 0};
+          t.kb = c, t.ks = 1, t.nk = dense_end - c + 1;
           pos = dense_end + 1;
         }
-        if (t.nk == kBN) {
-          bool full = true;
-          for (int32_t m = 0; m < nrows && full; ++m)
-            full = tile_row_bits(a.runs[rows[off + m]], t.kb, t.ks, t.nk) == ~0ull;
-          if (full) t.flags |= kTileFull;
+        t.mask_block = -1;
+        // per-row membership, per-wavefront state
+        uint64_t rb[kBM];
+        const uint64_t all = t.nk == 64 ? ~0ull : ((1ull << t.nk) - 1);
+        bool group_full = t.nk == kBN;
+        bool any_partial = false;
+        for (int32_t m = 0; m < kBM; ++m)
+          rb[m] = m < nrows ? tile_row_bits(a.runs[rows[off + m]], t.kb, t.ks, t.nk) : 0ull;
+        for (int32_t w = 0; w < kWavesPerGroup; ++w) {
+          bool full = t.nk == kBN, empty = true;
+          for (int32_t m = w * kWaveRows; m < (w + 1) * kWaveRows && m < nrows; ++m) {
+            full = full && rb[m] == all;
+            empty = empty && rb[m] == 0;
+          }
+          if (w * kWaveRows >= nrows) full = false;   // no real row: nothing to do
+          const int32_t st = empty ? kWaveEmpty : (full ? kWaveFull : kWavePartial);
+          t.flags |= st << (kWaveShift + 2 * w);
+          group_full = group_full && (st == kWaveFull || w * kWaveRows >= nrows);
+          any_partial = any_partial || st == kWavePartial;
+          if (st != kWaveEmpty) a.computed += int64_t(kWaveRows) * kBN;
+        }
+        if (group_full) t.flags |= kTileFull;
+        if (any_partial) {
+          t.mask_block = (int32_t)(a.masks.size() / kBM);
+          a.masks.insert(a.masks.end(), rb, rb + kBM);
         }
         p.t.push_back(t);
         if (pos >= L) break;
@@ -321,7 +342,6 @@ void plan_work(HostAcsr& a) {
     p.g.tile_begin = (int32_t)a.tiles.size();
     for (const Tile& t : p.t) {
       a.tiles.push_back(t);
-      a.computed += int64_t(kBM) * kBN;
       if (t.flags & kTileFull) ++a.n_full;
     }
     p.g.tile_end = (int32_t)a.tiles.size();

@@ -23,7 +23,8 @@ struct HostAcsr {
   std::vector<int32_t> rows;      // L, grouped
   std::vector<Group> groups;
   std::vector<Tile> tiles;
-  int64_t computed = 0;           // kBM * kBN per tile
+  std::vector<uint64_t> masks;    // kBM row masks per tile with a PARTIAL wavefront
+  int64_t computed = 0;           // kWaveRows * kBN per non-empty wavefront tile
   int32_t n_full = 0;
 };
 

@@ -56,7 +56,8 @@ splat_status upload(splat_acsr* h) {
   const size_t s_rows = al(sizeof(int32_t) * a.L);
   const size_t s_groups = al(sizeof(splat::Group) * a.groups.size());
   const size_t s_tiles = al(sizeof(splat::Tile) * (a.tiles.size() + 1));
-  const size_t total = s_rowptr + s_runs + s_rows + s_groups + s_tiles;
+  const size_t s_masks = al(sizeof(uint64_t) * (a.masks.size() + 1));
+  const size_t total = s_rowptr + s_runs + s_rows + s_groups + s_tiles + s_masks;
   void* mem = nullptr;
   e = hipMalloc(&mem, total);
   if (e != hipSuccess) {
@@ -71,9 +72,10 @@ splat_status upload(splat_acsr* h) {
                {a.runs.data(), sizeof(splat::RowRuns) * a.L, s_runs},
                {a.rows.data(), sizeof(int32_t) * a.L, s_rows},
                {a.groups.data(), sizeof(splat::Group) * a.groups.size(), s_groups},
-               {a.tiles.data(), sizeof(splat::Tile) * a.tiles.size(), s_tiles}};
-  char* dst[5];
-  for (int k = 0; k < 5; ++k) {
+               {a.tiles.data(), sizeof(splat::Tile) * a.tiles.size(), s_tiles},
+               {a.masks.data(), sizeof(uint64_t) * a.masks.size(), s_masks}};
+  char* dst[6];
+  for (int k = 0; k < 6; ++k) {
     dst[k] = p;
     if (parts[k].n) {
       e = hipMemcpy(p, parts[k].src, parts[k].n, hipMemcpyHostToDevice);
@@ -94,6 +96,7 @@ splat_status upload(splat_acsr* h) {
   h->dev.rows = (const int32_t*)dst[2];
   h->dev.groups = (const splat::Group*)dst[3];
   h->dev.tiles = (const splat::Tile*)dst[4];
+  h->dev.masks = (const uint64_t*)dst[5];
   return SPLAT_OK;
 }
 
@@ -278,10 +281,11 @@ splat_status splat_acsr_export_plan(splat_acsr_t h, int32_t* groups, int32_t* ro
   }
   std::memcpy(rows, a.rows.data(), sizeof(int32_t) * a.L);
   for (size_t t = 0; t < a.tiles.size(); ++t) {
-    tiles[4 * t] = a.tiles[t].kb;
-    tiles[4 * t + 1] = a.tiles[t].ks;
-    tiles[4 * t + 2] = a.tiles[t].nk;
-    tiles[4 * t + 3] = a.tiles[t].flags;
+    tiles[5 * t] = a.tiles[t].kb;
+    tiles[5 * t + 1] = a.tiles[t].ks;
+    tiles[5 * t + 2] = a.tiles[t].nk;
+    tiles[5 * t + 3] = a.tiles[t].flags;
+    tiles[5 * t + 4] = a.tiles[t].mask_block;
   }
   return ok();
 }

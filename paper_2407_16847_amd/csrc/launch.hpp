@@ -18,6 +18,7 @@ struct DevAcsr {
   const int32_t* rows;      // L (grouped)
   const Group* groups;      // n_groups
   const Tile* tiles;
+  const uint64_t* masks;    // kBM row masks per tile that has a PARTIAL wavefront
 };
 
 // Every launcher enqueues on `st` and returns the launch status.

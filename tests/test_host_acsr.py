@@ -70,15 +70,17 @@ def _check_against_mask(a, M):
 
 
 def _check_plan(a, M):
-    """Every non-zero is covered by exactly one (group, tile); FULL tiles are
-    full; tile keys are in range; each tile holds every column of its rows
-    inside its key interval; the exported per-row tile masks equal the mask."""
+    """Every non-zero is covered by exactly one (group, tile); tile keys are in
+    range and ascending; each tile holds every column of its rows inside its
+    key interval; the per-wavefront states (EMPTY / PARTIAL / FULL) and the
+    exported per-row tile masks equal the brute-force mask."""
     L = M.shape[0]
     info = a.info()
     groups, rows, tiles = a.export_plan()
     assert sorted(rows.tolist()) == list(range(L))
     assert info["bm"] == 128 and info["bn"] == 64
     covered = np.zeros_like(M, dtype=np.int32)
+    computed = 0
     prev_end = 0
     for g, (off, nrows, t0, t1) in enumerate(groups):
         assert 0 < nrows <= info["bm"] and t0 == prev_end and t1 >= t0
@@ -86,14 +88,29 @@ def _check_plan(a, M):
         grows = rows[off:off + nrows]
         last_hi = -1
         for t in range(t0, t1):
-            kb, ks, nk, flags = tiles[t]
+            kb, ks, nk, flags, mblock = tiles[t]
             assert 1 <= nk <= info["bn"] and ks >= 1
             keys = kb + ks * np.arange(nk)
             assert keys[0] >= 0 and keys[-1] < L and kb > last_hi   # ascending, disjoint
             last_hi = keys[-1]
             sub = M[np.ix_(grows, keys)]
-            if flags & 1:
-                assert nk == info["bn"] and sub.all()
+            any_partial = False
+            all_full = True
+            for w in range(4):
+                st = (flags >> (8 + 2 * w)) & 3
+                ws = sub[32 * w:32 * (w + 1)]
+                if ws.shape[0] == 0 or not ws.any():
+                    want = 0
+                elif nk == info["bn"] and ws.all():
+                    want = 3
+                else:
+                    want = 1
+                assert st == want, (g, t, w, st, want)
+                any_partial |= st == 1
+                all_full &= st == 3 or ws.shape[0] == 0
+                computed += 32 * 64 if st else 0
+            assert bool(flags & 1) == all_full
+            assert (mblock >= 0) == any_partial
             for m, i in enumerate(grows):
                 bits = a.tile_row_mask(t, int(i))
                 want = sum(1 << u for u in range(nk) if sub[m, u])
@@ -103,6 +120,7 @@ def _check_plan(a, M):
             covered[np.ix_(grows, keys)] += sub
     assert prev_end == len(tiles)
     assert (covered == M.astype(np.int32)).all()
+    assert computed == info["computed"]
     ntiles = np.array([g[3] - g[2] for g in groups])
     assert (np.diff(ntiles) <= 0).all()                      # heaviest groups first
 
