@@ -56,13 +56,19 @@ splat_status upload(splat_acsr* h) {
   const size_t s_rows = al(sizeof(int32_t) * a.L);
   const size_t s_groups = al(sizeof(splat::Group) * a.groups.size());
   const size_t s_tiles = al(sizeof(splat::Tile) * (a.tiles.size() + 1));
-  const size_t s_masks = al(sizeof(uint64_t) * (a.masks.size() + 1));
+  // one extra zero block: tiles without masks still issue (unused) mask loads
+  const size_t s_masks = al(sizeof(uint64_t) * (a.masks.size() + splat::kBM));
   const size_t total = s_rowptr + s_runs + s_rows + s_groups + s_tiles + s_masks;
   void* mem = nullptr;
   e = hipMalloc(&mem, total);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(SPLAT_ERR_OOM, "hipMalloc(%zu) for ACSR metadata: %s", total, hipGetErrorString(e));
+  }
+  e = hipMemset(mem, 0, total);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return fail(SPLAT_ERR_HIP, "hipMemset of ACSR metadata: %s", hipGetErrorString(e));
   }
   char* p = (char*)mem;
   struct Part {

@@ -4,8 +4,11 @@
 // softmax over each row's non-zeros), one workgroup per (row group, batch*head),
 // 4 wavefronts x 32 query rows.  For every planned key tile of its group:
 //
-//   1. K and V tiles [64 keys][d] -> LDS, double-buffered: the next tile's
-//      global loads are issued before the current tile is computed
+//   1. K and V tiles [64 keys][d] and the rows' tile masks travel from global
+//      memory straight into a ring of LDS slots (global_load_lds, no staging
+//      registers), issued NSLOT-1 tiles ahead; rows are stored unpadded with
+//      their 16-byte chunks XOR-swizzled so the MFMA operand reads below are
+//      free of bank conflicts
 //   2. S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q^T stays in registers); in this
 //      orientation each lane holds 32 scores of ONE query, so the row max and
 //      row sum need one exchange with lane ^ 32 only
@@ -31,6 +34,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
@@ -55,6 +59,49 @@ __device__ __forceinline__ bf16x4_t tr16(const __bf16* lds) {
   return __builtin_bit_cast(bf16x4_t, v);
 }
 
+// value of lane l ^ 32: one v_permlane32_swap of x with itself leaves the low
+// half's values in the first result and the high half's in the second
+__device__ __forceinline__ float lane_xor32(float x) {
+  const int xi = __builtin_bit_cast(int, x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(xi, xi, false, false);
+  const int lane = __lane_id();
+  return __builtin_bit_cast(float, lane < 32 ? sw[1] : sw[0]);
+}
+
+// The same transpose read issued as inline assembly: the compiler then does
+// not treat it as a possible reader of the in-flight global->LDS loads (it
+// would otherwise wait for all of them).  Its results are only valid after
+// lds_wait() below.
+__device__ __forceinline__ bf16x4_t tr16_async(unsigned lds_addr) {
+  i16x4_t v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(lds_addr));
+  return __builtin_bit_cast(bf16x4_t, v);
+}
+
+// Wait for every outstanding LDS read of this wavefront; the operands make the
+// values read by tr16_async depend on the wait.
+template <int NDB>
+__device__ __forceinline__ void lds_wait(bf16x8_t (*va)[4]);
+template <>
+__device__ __forceinline__ void lds_wait<2>(bf16x8_t (*va)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(va[0][0]), "+v"(va[0][1]), "+v"(va[0][2]), "+v"(va[0][3]), "+v"(va[1][0]),
+                 "+v"(va[1][1]), "+v"(va[1][2]), "+v"(va[1][3]));
+}
+template <>
+__device__ __forceinline__ void lds_wait<4>(bf16x8_t (*va)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(va[0][0]), "+v"(va[0][1]), "+v"(va[0][2]), "+v"(va[0][3]), "+v"(va[1][0]),
+                 "+v"(va[1][1]), "+v"(va[1][2]), "+v"(va[1][3]), "+v"(va[2][0]), "+v"(va[2][1]),
+                 "+v"(va[2][2]), "+v"(va[2][3]), "+v"(va[3][0]), "+v"(va[3][1]), "+v"(va[3][2]),
+                 "+v"(va[3][3]));
+}
+
+// 32-bit LDS address of a pointer into dynamic shared memory.
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
+}
+
 template <typename OutT>
 __device__ __forceinline__ void store4(OutT* p, float a, float b, float c, float d);
 template <>
@@ -67,32 +114,142 @@ __device__ __forceinline__ void store4<__bf16>(__bf16* p, float a, float b, floa
   *(bf16x4_t*)p = v;
 }
 
+constexpr int kDmaBytes = 16;                 // bytes per lane of one global->LDS load
+constexpr int kDmaBlock = 64 * kDmaBytes;     // bytes one wavefront load writes to LDS
+
+// Chunk swizzles.  K rows are read 32 rows x one 16-byte chunk per
+// instruction; V rows 4 rows x two chunks per 16 lanes (transpose reads).
+__device__ __forceinline__ int swz_k(int r) { return ((r >> 1) & 7) ^ ((r & 1) << 2); }
+__device__ __forceinline__ int swz_v(int r) { return (r & 3) << 1; }
+
+template <int D>
+struct Geo {
+  static constexpr int RB = 2 * D;                      // bytes per K/V row in LDS
+  static constexpr int CPR = RB / 16;                   // 16-byte chunks per row
+  static constexpr int TB = kBN * RB;                   // bytes of a K (or V) tile
+  static constexpr int NBW = TB / kDmaBlock / 4;        // loads per wavefront per tile
+  static constexpr int RPB = kDmaBlock / RB;            // rows per load
+  static constexpr int SLOT = 2 * TB + kBM * 8;         // K tile, V tile, row masks
+  static constexpr int NSLOT = D == 64 ? 3 : 2;         // ring depth
+  static constexpr int OPS = 2 * NBW + 1;               // vector-memory ops per wavefront per tile
+  static constexpr int LDS = NSLOT * SLOT;
+  static constexpr int NKS = D / 16, NDB = D / 32;
+};
+
+__device__ __forceinline__ void dma16(const void* g, char* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, kDmaBytes, 0, 0);
+}
+
+// Issue this wavefront's share of one tile's global->LDS loads into a slot.
+// Keys past the tile's end re-read its last key (finite data the masks
+// exclude).  The 16 lanes of the mask load bring the wavefront's 32 row masks.
+template <int D>
+__device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf16* Kh,
+                                           const __bf16* Vh, const uint64_t* masks, int wave,
+                                           int lane) {
+  using G = Geo<D>;
+  const int last = tl.nk - 1;
+#pragma unroll
+  for (int k = 0; k < G::NBW; ++k) {
+    const int bk = wave + 4 * k;
+    const int r = bk * G::RPB + lane / G::CPR;
+    const int pos = lane % G::CPR;
+    const size_t row = (size_t)(tl.kb + tl.ks * min(r, last)) * D;
+    dma16(Kh + row + 8 * (pos ^ swz_k(r)), slot + bk * kDmaBlock);
+    dma16(Vh + row + 8 * (pos ^ swz_v(r)), slot + G::TB + bk * kDmaBlock);
+  }
+  const uint64_t* mrow = masks + (size_t)max(tl.mask_block, 0) * kBM + wave * 32 + 2 * lane;
+  if (lane < 16) dma16(mrow, slot + 2 * G::TB + wave * 256);
+}
+
+// Wait until at most `pending` vector-memory ops of this wavefront are
+// outstanding and all of its LDS reads are done, then barrier.  The empty asm
+// statements keep the compiler from moving LDS accesses across it.
+template <int PENDING>
+__device__ __forceinline__ void ring_sync() {
+  static_assert(PENDING < 64, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((PENDING & 15) | ((PENDING >> 4) << 14) | (7 << 4));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Online-softmax step of one tile for this lane's row: optional mask, tile
+// max, lazy update of the running max (only when a score exceeds it by more
+// than 2^kRescaleThreshold), p = exp2(s * scale*log2(e) - m) rounded to bf16
+// into the P^T operand, running sum of the rounded p.  alpha is the factor the
+// output accumulator must be scaled by before this tile's P V is added;
+// the return value says whether any lane of the wavefront needs it.
+template <bool MASKED>
+__device__ __forceinline__ bool tile_softmax(f32x16_t* s, uint64_t mk, int h, float sl2,
+                                             float& m_run, float& l_run, float& alpha,
+                                             bf16x8_t* pf) {
+  if (MASKED) {
+    const uint64_t bits = mk >> (4 * h);
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int u = 32 * kb2 + 8 * (r >> 2) + (r & 3);
+        if (!((bits >> u) & 1ull)) s[kb2][r] = -INFINITY;
+      }
+  }
+  float mx0 = -INFINITY, mx1 = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    mx0 = fmaxf(mx0, s[0][r]);
+    mx1 = fmaxf(mx1, s[1][r]);
+  }
+  float mx = fmaxf(mx0, mx1);
+  mx = fmaxf(mx, lane_xor32(mx));
+  const float m_new = fmaxf(m_run, mx * sl2);
+  const bool need = m_new > m_run + kRescaleThreshold;
+  alpha = need ? exp2_hw(m_run - m_new) : 1.f;   // exp2(-inf) = 0 on the first tile
+  m_run = need ? m_new : m_run;
+  l_run *= alpha;
+  const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
+  float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      pf[j][e] = (__bf16)exp2_hw(fmaf(s[j >> 1][(j & 1) * 8 + e], sl2, neg_m));
+    // row sum of the bf16-rounded p, two at a time, two partial sums
+#pragma unroll
+    for (int e = 0; e < 8; e += 4) {
+      const bf16x2_t p0 = {pf[j][e], pf[j][e + 1]};
+      const bf16x2_t p1 = {pf[j][e + 2], pf[j][e + 3]};
+      l0 = __builtin_amdgcn_fdot2_f32_bf16(p0, kOnes2, l0, false);
+      l1 = __builtin_amdgcn_fdot2_f32_bf16(p1, kOnes2, l1, false);
+    }
+  }
+  l_run += l0 + l1;
+  return __any(need);
+}
+
+// The plan arrays are kernel arguments of their own, const and __restrict__,
+// so their (wavefront-uniform) reads are scalar loads, independent of the
+// vector-memory counter that tracks the global->LDS loads.
 template <int D, typename OutT>
-__global__ __launch_bounds__(kThreads, D == 64 ? 4 : 1) void k_fused_mfma(DevAcsr a, int BH,
-                                                            const __bf16* __restrict__ Q,
-                                                            const __bf16* __restrict__ K,
-                                                            const __bf16* __restrict__ V, float sl2,
-                                                            OutT* __restrict__ O) {
-  constexpr int BN = kBN;
-  constexpr int P = D + 8;        // K and V tile row pitch (elements): 16-byte aligned rows
-  constexpr int CPR = D / 8;      // 16-byte chunks per K/V row
-  constexpr int CPT = BN * CPR / kThreads;  // chunks per thread per tile
-  constexpr int NKS = D / 16;     // k-steps of the QK^T product
-  constexpr int NDB = D / 32;     // 32-wide feature blocks of O
-  static_assert(CPT * kThreads == BN * CPR, "tile chunks must divide evenly");
-  __shared__ __attribute__((aligned(16))) __bf16 sK[2][BN * P];
-  __shared__ __attribute__((aligned(16))) __bf16 sV[2][BN * P];
+__global__ __launch_bounds__(kThreads, D == 64 ? 3 : 2) void k_fused_mfma(
+    const Group* __restrict__ groups, const int32_t* __restrict__ rows,
+    const Tile* __restrict__ tiles, const uint64_t* __restrict__ masks, int L, int BH,
+    const __bf16* __restrict__ Q, const __bf16* K, const __bf16* V, float sl2,
+    OutT* __restrict__ O) {
+  using G = Geo<D>;
+  constexpr int NKS = G::NKS, NDB = G::NDB, NSLOT = G::NSLOT, RB = G::RB;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
 
   const int g = blockIdx.x / BH;
   const int bh = blockIdx.x - g * BH;
-  const Group grp = a.groups[g];
+  const Group grp = groups[g];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int qi = lane & 31, h = lane >> 5;
   const int m = wave * 32 + qi;
   const bool row_valid = m < grp.nrows;
-  const int row = row_valid ? a.rows[grp.row_off + m] : 0;
-  const size_t head = (size_t)bh * a.L * D;
+  const int row = row_valid ? rows[grp.row_off + m] : 0;
+  const size_t head = (size_t)bh * L * D;
   const __bf16* Kh = K + head;
   const __bf16* Vh = V + head;
 
@@ -110,11 +267,22 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 1) void k_fused_mfma(DevAcs
       }
     }
   }
+  // K operand of key row r = 32*kb2 + qi, chunk 2*ks + h (swizzle depends on r % 16)
+  int koff[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks)
+    koff[ks] = qi * RB + 16 * ((((2 * ks + h) & 7) ^ swz_k(qi)) | ((2 * ks + h) & ~7));
   // V^T operand by LDS transpose reads: within each 16-lane group, lane i
-  // addresses row k0 + i/4, features d0 + 4*(i%4) .. +3 and receives
-  // V[k0 + 0..3][d0 + i]; k0 = 4*h, d0 = 16 * (lane/16 % 2)
-  const int voff = (4 * h + ((lane & 15) >> 2)) * P + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int koff = qi * P + h * 8;
+  // addresses key row 4*h + i/4 (+ 16*j, + 8), features 32*b + 16*(lane/16 % 2)
+  // + 4*(i%4) .. +3, and receives V[4 rows][feature 32*b + lane%32]
+  int voff[NDB];
+  {
+    const int i = lane & 15;
+    const int rv = 4 * h + (i >> 2);
+    const int cl = 2 * ((lane >> 4) & 1) + ((i & 3) >> 1);
+#pragma unroll
+    for (int b = 0; b < NDB; ++b) voff[b] = rv * RB + 16 * ((4 * b + cl) ^ swz_v(rv)) + 8 * (i & 1);
+  }
 
   f32x16_t oacc[NDB];
 #pragma unroll
@@ -123,123 +291,84 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 1) void k_fused_mfma(DevAcs
     for (int r = 0; r < 16; ++r) oacc[b][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // K/V tile staging: global -> registers (issued one tile ahead) -> LDS
-  uint4 pk[CPT], pv[CPT];
-  auto gload = [&](const Tile& tl) {
+  const int tb = grp.tile_begin, nt = grp.tile_end - grp.tile_begin;
+  if (nt > 0) {
+    // prologue: the first NSLOT-1 tiles
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * kThreads;
-      const int u = c / CPR, dc = (c % CPR) * 8;
-      pk[i] = make_uint4(0u, 0u, 0u, 0u);
-      pv[i] = pk[i];
-      if (u < tl.nk) {
-        const size_t off = (size_t)(tl.kb + tl.ks * u) * D + dc;
-        pk[i] = *(const uint4*)(Kh + off);
-        pv[i] = *(const uint4*)(Vh + off);
-      }
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * kThreads;
-      const int u = c / CPR, dc = (c % CPR) * 8;
-      *(uint4*)(&sK[buf][u * P + dc]) = pk[i];
-      *(uint4*)(&sV[buf][u * P + dc]) = pv[i];
-    }
-  };
+    for (int sl = 0; sl < NSLOT - 1; ++sl)
+      issue_tile<D>(smem + sl * G::SLOT, tiles[tb + min(sl, nt - 1)], Kh, Vh, masks, wave, lane);
+    // descriptors are read one iteration before they are needed
+    Tile next_issue = tiles[tb + min(NSLOT - 1, nt - 1)];
+    int next_flags = tiles[tb].flags;
+    ring_sync<0>();
 
-  if (grp.tile_begin < grp.tile_end) {
-    gload(a.tiles[grp.tile_begin]);
-    sstore(0);
-  }
-  __syncthreads();
-
-  for (int t = grp.tile_begin; t < grp.tile_end; ++t) {
-    const int buf = (t - grp.tile_begin) & 1;
-    const Tile tl = a.tiles[t];
-    // this wavefront's 32 rows: no key in the tile / some (precomputed
-    // per-row masks) / every key
-    const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
-    uint64_t bits = ~0ull;
-    if (wst == kWavePartial) bits = a.masks[(size_t)tl.mask_block * kBM + m] >> (4 * h);
-    const bool has_next = t + 1 < grp.tile_end;
-    if (has_next) gload(a.tiles[t + 1]);
-    if (wst != kWaveEmpty) {
-      const __bf16* cK = sK[buf];
-      const __bf16* cV = sV[buf];
-
-      // S^T[key][query] for the tile's two 32-key blocks
-      f32x16_t sacc[2];
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[kb2][r] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const bf16x8_t ka = *(const bf16x8_t*)(cK + kb2 * 32 * P + koff + ks * 16);
-          sacc[kb2] = mfma32(ka, qf[ks], sacc[kb2]);
-        }
-      }
-      // sacc[kb2][r] is the score of key u = 32*kb2 + 8*(r/4) + 4*h + r%4
-      if (wst == kWavePartial) {
+    for (int i = 0; i < nt; ++i) {
+      const int t = tb + i;
+      char* cur = smem + (i % NSLOT) * G::SLOT;
+      const Tile to_issue = next_issue;
+      const int flags = next_flags;
+      next_issue = tiles[tb + min(i + NSLOT, nt - 1)];
+      next_flags = tiles[tb + min(i + 1, nt - 1)].flags;
+      issue_tile<D>(smem + ((i + NSLOT - 1) % NSLOT) * G::SLOT, to_issue, Kh, Vh, masks, wave,
+                    lane);
+      const int wst = (flags >> (kWaveShift + 2 * wave)) & 3;
+      if (wst != kWaveEmpty) {
+        const __bf16* cK = (const __bf16*)cur;
+        const __bf16* cV = (const __bf16*)(cur + G::TB);
+        // S^T[key][query]: all K operands read, then the products
+        bf16x8_t ka[2][NKS];
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int u = 32 * kb2 + 8 * (r >> 2) + (r & 3);
-            if (!((bits >> u) & 1ull)) sacc[kb2][r] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
+          for (int ks = 0; ks < NKS; ++ks)
+            ka[kb2][ks] = *(const bf16x8_t*)((const char*)cK + kb2 * 32 * RB + koff[ks]);
+        f32x16_t sacc[2];
 #pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2)
+        for (int kb2 = 0; kb2 < 2; ++kb2) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb2][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx * sl2);
-      if (__any(m_new > m_run + kRescaleThreshold)) {
-        const float alpha = (m_new == -INFINITY) ? 1.f : exp2_hw(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
+          for (int r = 0; r < 16; ++r) sacc[kb2][r] = 0.f;
+#pragma unroll
+          for (int ks = 0; ks < NKS; ++ks) sacc[kb2] = mfma32(ka[kb2][ks], qf[ks], sacc[kb2]);
+        }
+        float alpha;
+        bf16x8_t pf[4];
+        bool need;
+        if (wst == kWavePartial) {
+          const uint64_t mk = *(const uint64_t*)(cur + 2 * G::TB + m * 8);
+          need = tile_softmax<true>(sacc, mk, h, sl2, m_run, l_run, alpha, pf);
+        } else {
+          need = tile_softmax<false>(sacc, 0, h, sl2, m_run, l_run, alpha, pf);
+        }
+        if (need) {
+#pragma unroll
+          for (int b = 0; b < NDB; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[b][r] *= alpha;
+        }
+        // O^T[d][query] += V^T[d][key] P^T[key][query]; k-step j, element e of
+        // lane half h is key 16*j + 8*(e/4) + 4*h + e%4
+        bf16x8_t va[NDB][4];
+        const unsigned vbase = lds_addr(cV);
 #pragma unroll
         for (int b = 0; b < NDB; ++b)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[b][r] *= alpha;
+          for (int j = 0; j < 4; ++j) {
+            const unsigned vp = vbase + voff[b] + 16 * j * RB;
+            va[b][j] = __builtin_shufflevector(tr16_async(vp), tr16_async(vp + 8 * RB), 0, 1, 2,
+                                               3, 4, 5, 6, 7);
+          }
+        lds_wait<NDB>(va);
+#pragma unroll
+        for (int b = 0; b < NDB; ++b)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) oacc[b] = mfma32(va[b][j], pf[j], oacc[b]);
       }
-      const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
-      bf16x8_t pf[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          pf[j][e] = (__bf16)exp2_hw(fmaf(sacc[j >> 1][(j & 1) * 8 + e], sl2, neg_m));
-        // row sum of the bf16-rounded p, two at a time
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const bf16x2_t pair = {pf[j][e], pf[j][e + 1]};
-          l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, kOnes2, l_run, false);
-        }
-      }
-      // O^T[d][query] += V^T[d][key] P^T[key][query]; k-step j, element e of lane
-      // half h is key 16*j + 8*(e/4) + 4*h + e%4
-#pragma unroll
-      for (int b = 0; b < NDB; ++b) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const __bf16* vp = cV + voff + 16 * j * P + 32 * b;
-          const bf16x4_t lo = tr16(vp);
-          const bf16x4_t hi = tr16(vp + 8 * P);
-          const bf16x8_t va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          oacc[b] = mfma32(va, pf[j], oacc[b]);
-        }
-      }
+      // the next tile's loads (issued NSLOT-2 tiles ago) have landed
+      ring_sync<G::OPS * (NSLOT - 2)>();
     }
-    if (has_next) sstore(buf ^ 1);
-    __syncthreads();
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = l_run + lane_xor32(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (row_valid) {
     OutT* orow = O + head + (size_t)row * D;
@@ -254,17 +383,28 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 1) void k_fused_mfma(DevAcs
   }
 }
 
+template <int D, typename OutT>
+hipError_t fused_launch(const DevAcsr& a, int BH, const void* Q, const void* K, const void* V,
+                        float sl2, void* O, hipStream_t st) {
+  constexpr int lds = Geo<D>::LDS;
+  static bool attr_set = false;   // the LDS size attribute is per kernel, set once
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute((const void*)k_fused_mfma<D, OutT>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((k_fused_mfma<D, OutT>), dim3(a.n_groups * BH), dim3(kThreads), lds, st,
+                     a.groups, a.rows, a.tiles, a.masks, a.L, BH, (const __bf16*)Q,
+                     (const __bf16*)K, (const __bf16*)V, sl2, (OutT*)O);
+  return hipGetLastError();
+}
+
 template <int D>
 hipError_t fused_d(const DevAcsr& a, int BH, const void* Q, const void* K, const void* V,
                    float sl2, void* O, int out_dtype, hipStream_t st) {
-  const dim3 grid(a.n_groups * BH), block(kThreads);
-  if (out_dtype == 0)
-    hipLaunchKernelGGL((k_fused_mfma<D, float>), grid, block, 0, st, a, BH, (const __bf16*)Q,
-                       (const __bf16*)K, (const __bf16*)V, sl2, (float*)O);
-  else
-    hipLaunchKernelGGL((k_fused_mfma<D, __bf16>), grid, block, 0, st, a, BH, (const __bf16*)Q,
-                       (const __bf16*)K, (const __bf16*)V, sl2, (__bf16*)O);
-  return hipGetLastError();
+  return out_dtype == 0 ? fused_launch<D, float>(a, BH, Q, K, V, sl2, O, st)
+                        : fused_launch<D, __bf16>(a, BH, Q, K, V, sl2, O, st);
 }
 
 }  // namespace
