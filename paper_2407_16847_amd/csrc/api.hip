@@ -96,6 +96,7 @@ splat_status upload(splat_acsr* h) {
   h->device = dev;
   h->dev.L = a.L;
   h->dev.nnz = a.nnz;
+  h->dev.max_row_nnz = a.max_row_nnz;
   h->dev.n_groups = (int32_t)a.groups.size();
   h->dev.row_ptr = (const int32_t*)dst[0];
   h->dev.runs = (const splat::RowRuns*)dst[1];
@@ -315,9 +316,10 @@ splat_status splat_rsddmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t 
   CHECK(check_ptr(K, "K"));
   if (h->host.nnz == 0) return ok();
   CHECK(check_ptr(S, "S"));
-  return launched(splat::launch_rsddmm_rows(h->dev, dtype, B * H, d, Q, K, scale, S,
-                                            (hipStream_t)stream),
-                  "rsddmm");
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == SPLAT_BF16)
+    return launched(splat::launch_rsddmm_tiles(h->dev, B * H, d, Q, K, scale, S, st), "rsddmm");
+  return launched(splat::launch_rsddmm_rows(h->dev, dtype, B * H, d, Q, K, scale, S, st), "rsddmm");
 }
 
 splat_status splat_row_softmax(splat_acsr_t h, int32_t B, int32_t H, const float* S, float* P,
@@ -330,7 +332,10 @@ splat_status splat_row_softmax(splat_acsr_t h, int32_t B, int32_t H, const float
   const char *s0 = (const char*)S, *p0 = (const char*)P;
   if (s0 != p0 && s0 < p0 + bytes && p0 < s0 + bytes)
     return fail(SPLAT_ERR_INVALID_ARG, "S and P overlap without being equal");
-  return launched(splat::launch_softmax_rows(h->dev, B * H, S, P, (hipStream_t)stream), "row_softmax");
+  hipStream_t st = (hipStream_t)stream;
+  if (splat::softmax_regs_fits(h->dev))
+    return launched(splat::launch_softmax_regs(h->dev, B * H, S, P, st), "row_softmax");
+  return launched(splat::launch_softmax_rows(h->dev, B * H, S, P, st), "row_softmax");
 }
 
 splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
@@ -342,9 +347,10 @@ splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H
   if (h->host.nnz > 0) CHECK(check_ptr(P, "P"));
   CHECK(check_ptr(V, "V"));
   CHECK(check_ptr(O, "O"));
-  return launched(splat::launch_rspmm_rows(h->dev, dtype, B * H, d, P, V, O, out_dtype,
-                                           (hipStream_t)stream),
-                  "rspmm");
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == SPLAT_BF16)
+    return launched(splat::launch_rspmm_tiles(h->dev, B * H, d, P, V, O, out_dtype, st), "rspmm");
+  return launched(splat::launch_rspmm_rows(h->dev, dtype, B * H, d, P, V, O, out_dtype, st), "rspmm");
 }
 
 splat_status splat_sparse_mhsa_fwd(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,

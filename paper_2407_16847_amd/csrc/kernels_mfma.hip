@@ -27,100 +27,15 @@
 #include <math.h>
 
 #include "launch.hpp"
+#include "mfma_util.hpp"
 
 namespace splat {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
-
-constexpr bf16x2_t kOnes2 = {(__bf16)1.f, (__bf16)1.f};
+using namespace mfma;
 
 constexpr int kThreads = 256;           // 4 waves
 constexpr float kRescaleThreshold = 8.f; // log2 units
-
-__device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// LDS transpose read (ds_read_b64_tr_b16): within each group of 16 lanes, lane
-// i receives element i%4 of the 8-byte chunks addressed by lanes i/4, 4 + i/4,
-// 8 + i/4 and 12 + i/4 -- a 4 x 16 block of 16-bit values read transposed.
-__device__ __forceinline__ bf16x4_t tr16(const __bf16* lds) {
-  const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4_t*)(__attribute__((address_space(3))) __bf16*)(lds));
-  return __builtin_bit_cast(bf16x4_t, v);
-}
-
-// value of lane l ^ 32: one v_permlane32_swap of x with itself leaves the low
-// half's values in the first result and the high half's in the second
-__device__ __forceinline__ float lane_xor32(float x) {
-  const int xi = __builtin_bit_cast(int, x);
-  const auto sw = __builtin_amdgcn_permlane32_swap(xi, xi, false, false);
-  const int lane = __lane_id();
-  return __builtin_bit_cast(float, lane < 32 ? sw[1] : sw[0]);
-}
-
-// The same transpose read issued as inline assembly: the compiler then does
-// not treat it as a possible reader of the in-flight global->LDS loads (it
-// would otherwise wait for all of them).  Its results are only valid after
-// lds_wait() below.
-__device__ __forceinline__ bf16x4_t tr16_async(unsigned lds_addr) {
-  i16x4_t v;
-  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(lds_addr));
-  return __builtin_bit_cast(bf16x4_t, v);
-}
-
-// Wait for every outstanding LDS read of this wavefront; the operands make the
-// values read by tr16_async depend on the wait.
-template <int NDB>
-__device__ __forceinline__ void lds_wait(bf16x8_t (*va)[4]);
-template <>
-__device__ __forceinline__ void lds_wait<2>(bf16x8_t (*va)[4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)"
-               : "+v"(va[0][0]), "+v"(va[0][1]), "+v"(va[0][2]), "+v"(va[0][3]), "+v"(va[1][0]),
-                 "+v"(va[1][1]), "+v"(va[1][2]), "+v"(va[1][3]));
-}
-template <>
-__device__ __forceinline__ void lds_wait<4>(bf16x8_t (*va)[4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)"
-               : "+v"(va[0][0]), "+v"(va[0][1]), "+v"(va[0][2]), "+v"(va[0][3]), "+v"(va[1][0]),
-                 "+v"(va[1][1]), "+v"(va[1][2]), "+v"(va[1][3]), "+v"(va[2][0]), "+v"(va[2][1]),
-                 "+v"(va[2][2]), "+v"(va[2][3]), "+v"(va[3][0]), "+v"(va[3][1]), "+v"(va[3][2]),
-                 "+v"(va[3][3]));
-}
-
-// 32-bit LDS address of a pointer into dynamic shared memory.
-__device__ __forceinline__ unsigned lds_addr(const void* p) {
-  return (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
-}
-
-template <typename OutT>
-__device__ __forceinline__ void store4(OutT* p, float a, float b, float c, float d);
-template <>
-__device__ __forceinline__ void store4<float>(float* p, float a, float b, float c, float d) {
-  *(float4*)p = make_float4(a, b, c, d);
-}
-template <>
-__device__ __forceinline__ void store4<__bf16>(__bf16* p, float a, float b, float c, float d) {
-  bf16x4_t v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
-  *(bf16x4_t*)p = v;
-}
-
-constexpr int kDmaBytes = 16;                 // bytes per lane of one global->LDS load
-constexpr int kDmaBlock = 64 * kDmaBytes;     // bytes one wavefront load writes to LDS
-
-// Chunk swizzles.  K rows are read 32 rows x one 16-byte chunk per
-// instruction; V rows 4 rows x two chunks per 16 lanes (transpose reads).
-__device__ __forceinline__ int swz_k(int r) { return ((r >> 1) & 7) ^ ((r & 1) << 2); }
-__device__ __forceinline__ int swz_v(int r) { return (r & 3) << 1; }
 
 template <int D>
 struct Geo {
@@ -136,9 +51,6 @@ struct Geo {
   static constexpr int NKS = D / 16, NDB = D / 32;
 };
 
-__device__ __forceinline__ void dma16(const void* g, char* lds) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, kDmaBytes, 0, 0);
-}
 
 // Issue this wavefront's share of one tile's global->LDS loads into a slot.
 // Keys past the tile's end re-read its last key (finite data the masks
@@ -160,18 +72,6 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
   }
   const uint64_t* mrow = masks + (size_t)max(tl.mask_block, 0) * kBM + wave * 32 + 2 * lane;
   if (lane < 16) dma16(mrow, slot + 2 * G::TB + wave * 256);
-}
-
-// Wait until at most `pending` vector-memory ops of this wavefront are
-// outstanding and all of its LDS reads are done, then barrier.  The empty asm
-// statements keep the compiler from moving LDS accesses across it.
-template <int PENDING>
-__device__ __forceinline__ void ring_sync() {
-  static_assert(PENDING < 64, "vmcnt field");
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt((PENDING & 15) | ((PENDING >> 4) << 14) | (7 << 4));
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 // Online-softmax step of one tile for this lane's row: optional mask, tile
@@ -272,17 +172,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 3 : 2) void k_fused_mfma(
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks)
     koff[ks] = qi * RB + 16 * ((((2 * ks + h) & 7) ^ swz_k(qi)) | ((2 * ks + h) & ~7));
-  // V^T operand by LDS transpose reads: within each 16-lane group, lane i
-  // addresses key row 4*h + i/4 (+ 16*j, + 8), features 32*b + 16*(lane/16 % 2)
-  // + 4*(i%4) .. +3, and receives V[4 rows][feature 32*b + lane%32]
+  // V^T operand by LDS transpose reads
   int voff[NDB];
-  {
-    const int i = lane & 15;
-    const int rv = 4 * h + (i >> 2);
-    const int cl = 2 * ((lane >> 4) & 1) + ((i & 3) >> 1);
-#pragma unroll
-    for (int b = 0; b < NDB; ++b) voff[b] = rv * RB + 16 * ((4 * b + cl) ^ swz_v(rv)) + 8 * (i & 1);
-  }
+  v_operand_offsets<D>(lane, voff);
 
   f32x16_t oacc[NDB];
 #pragma unroll
@@ -303,7 +195,6 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 3 : 2) void k_fused_mfma(
     ring_sync<0>();
 
     for (int i = 0; i < nt; ++i) {
-      const int t = tb + i;
       char* cur = smem + (i % NSLOT) * G::SLOT;
       const Tile to_issue = next_issue;
       const int flags = next_flags;
@@ -348,16 +239,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 3 : 2) void k_fused_mfma(
         // O^T[d][query] += V^T[d][key] P^T[key][query]; k-step j, element e of
         // lane half h is key 16*j + 8*(e/4) + 4*h + e%4
         bf16x8_t va[NDB][4];
-        const unsigned vbase = lds_addr(cV);
-#pragma unroll
-        for (int b = 0; b < NDB; ++b)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const unsigned vp = vbase + voff[b] + 16 * j * RB;
-            va[b][j] = __builtin_shufflevector(tr16_async(vp), tr16_async(vp + 8 * RB), 0, 1, 2,
-                                               3, 4, 5, 6, 7);
-          }
-        lds_wait<NDB>(va);
+        read_v_operands<D>(lds_addr(cV), voff, va);
 #pragma unroll
         for (int b = 0; b < NDB; ++b)
 #pragma unroll

@@ -1,0 +1,397 @@
+// kernels_tiles.hip -- the unfused chain of Equation 1 for bf16 inputs, over the
+// tile plan: R-SDDMM on the matrix cores, the row softmax with each row held
+// in registers, and R-SpMM on the matrix cores.  S and P are fp32 in the
+// ACSR value order (row i's values at row_ptr[i] .. row_ptr[i+1], ascending
+// column).
+//
+// Position of a tile element in its row.  The tiles of a row group cover
+// disjoint, ascending column intervals and every column of the group's rows
+// lies in exactly one of them, so a row's values for tile t start right after
+// its values for tiles 0 .. t-1: each lane keeps a running count `cnt` of its
+// row's columns in the tiles already passed, and key u of tile t sits at
+//     row_ptr[i] + cnt + popcount(rowbits & ((1 << u) - 1)),
+// rowbits being the row's membership mask in the tile (all ones for a
+// wavefront the plan marks FULL, the stored 64-bit mask for PARTIAL).  No
+// run arithmetic and no division is needed on the device.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "launch.hpp"
+#include "mfma_util.hpp"
+
+namespace splat {
+namespace {
+
+using namespace mfma;
+
+constexpr int kTileThreads = 256;   // 4 wavefronts x 32 rows of a group
+
+// 4 floats at a 4-byte aligned address (values of a row start anywhere)
+typedef float f32x4u_t __attribute__((ext_vector_type(4), aligned(4)));
+
+__device__ __forceinline__ int popc64(uint64_t x) { return __builtin_popcountll(x); }
+
+// The keys a lane of half h holds in both MFMA layouts used here come in
+// eight groups of four: keys 8*g + 4*h + e (g < 8, e < 4).  For a row's
+// membership mask `bits` in a tile, f(g, e, present, pos) is called for each
+// of them with `pos` the key's position among the row's keys of the tile
+// (meaningful when present).  Only constant shifts are used, so nothing
+// lane-dependent is kept live across the tile loop.
+template <typename F>
+__device__ __forceinline__ void for_each_key(uint64_t bits, int h, F&& f) {
+  const uint64_t b = bits >> (4 * h);
+  int off = h ? __builtin_popcount((uint32_t)bits & 0xFu) : 0;
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    const uint32_t nib = (uint32_t)(b >> (8 * g)) & 0xFu;
+    const uint32_t oth = (uint32_t)(b >> (8 * g + 4)) & 0xFu;   // the other half's next four
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f(g, e, (nib >> e) & 1u, off + __builtin_popcount(nib & ((1u << e) - 1u)));
+    off += __builtin_popcount(nib) + __builtin_popcount(oth);
+  }
+}
+
+// --------------------------------------------------------------------------
+// R-SDDMM: S[b,h,row_ptr[i] + k] = scale * <Q[b,h,i,:], K[b,h,col(i,k),:]>.
+// One workgroup per (row group, batch*head).  Per key tile a wavefront forms
+// S^T = K Q^T for its 32 rows on v_mfma_f32_32x32x16_bf16 with both operands
+// read straight from global memory (16 bytes per lane; the 4 wavefronts of a
+// group read the same K tile, which stays in cache), then stores the scores
+// of the row's columns.  Lane (qi, h) holds keys 32*kb2 + 8*(r/4) + 4*h + r%4
+// of query row qi, so on FULL tiles it writes 4 consecutive values at a time.
+template <int D>
+__global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
+    const Group* __restrict__ groups, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ row_ptr, const Tile* __restrict__ tiles,
+    const uint64_t* __restrict__ masks, int L, int BH, int64_t nnz,
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, float scale,
+    float* __restrict__ S) {
+  constexpr int NKS = D / 16;
+  const int g = blockIdx.x / BH;
+  const int bh = blockIdx.x - g * BH;
+  const Group grp = groups[g];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (wave * kWaveRows >= grp.nrows) return;   // no barriers below
+  const int qi = lane & 31, h = lane >> 5;
+  const int m = wave * kWaveRows + qi;
+  const bool row_valid = m < grp.nrows;
+  const int row = row_valid ? rows[grp.row_off + m] : 0;
+  const size_t head = (size_t)bh * L * D;
+  const __bf16* Kh = K + head;
+
+  bf16x8_t qf[NKS];
+  {
+    const __bf16* qrow = Q + head + (size_t)row * D;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      if (row_valid) {
+        qf[ks] = *(const bf16x8_t*)(qrow + ks * 16 + h * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[ks][e] = (__bf16)0.f;
+      }
+    }
+  }
+  float* srow = S + (size_t)bh * nnz + row_ptr[row];
+  int cnt = 0;
+
+  for (int t = grp.tile_begin; t < grp.tile_end; ++t) {
+    const Tile tl = tiles[t];
+    const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
+    if (wst == kWaveEmpty) continue;
+    const int last = tl.nk - 1;
+    bf16x8_t ka[2][NKS];
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2) {
+      const __bf16* krow = Kh + (size_t)(tl.kb + tl.ks * min(32 * kb2 + qi, last)) * D + 8 * h;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) ka[kb2][ks] = *(const bf16x8_t*)(krow + 16 * ks);
+    }
+    const uint64_t bits =
+        wst == kWaveFull ? ~0ull : masks[(size_t)max(tl.mask_block, 0) * kBM + m];
+    f32x16_t sacc[2];
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[kb2][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) sacc[kb2] = mfma32(ka[kb2][ks], qf[ks], sacc[kb2]);
+    }
+    if (row_valid) {
+      float* dst = srow + cnt;
+      if (wst == kWaveFull) {
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            const f32x4u_t v = {sacc[kb2][4 * rg] * scale, sacc[kb2][4 * rg + 1] * scale,
+                                sacc[kb2][4 * rg + 2] * scale, sacc[kb2][4 * rg + 3] * scale};
+            *(f32x4u_t*)(dst + 32 * kb2 + 8 * rg + 4 * h) = v;
+          }
+      } else {
+        // key 8*g + 4*h + e is element 4*(g%4) + e of sacc[g/4]
+        for_each_key(bits, h, [&](int g, int e, unsigned present, int pos) {
+          if (present) dst[pos] = sacc[g >> 2][4 * (g & 3) + e] * scale;
+        });
+      }
+    }
+    cnt += popc64(bits);
+  }
+}
+
+// --------------------------------------------------------------------------
+// Row softmax over the non-zeros (section 6): one wavefront per (batch*head,
+// row), the row's values held in registers (4 consecutive values per lane
+// and load, NV loads), so S is read once and P written once.  P may alias S:
+// every value is read before any is written, each by the lane that writes it.
+template <int NV>
+__global__ __launch_bounds__(256) void k_softmax_regs(const int32_t* __restrict__ row_ptr, int L,
+                                                      int64_t n_rows, int64_t nnz, const float* S,
+                                                      float* P) {
+  constexpr float kLog2e = 1.4426950408889634f;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + wave;
+  if (r >= n_rows) return;
+  const int bh = (int)(r / L);
+  const int i = (int)(r - (int64_t)bh * L);
+  const int32_t b0 = row_ptr[i];
+  const int n = row_ptr[i + 1] - b0;
+  if (n == 0) return;
+  const size_t base = (size_t)bh * nnz + b0;
+  const float* s = S + base;
+  float* p = P + base;
+
+  float x[NV][4];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int idx = 4 * (lane + 64 * k);
+    if (idx + 3 < n) {
+      const f32x4u_t v = *(const f32x4u_t*)(s + idx);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[k][e] = v[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[k][e] = idx + e < n ? s[idx + e] : -INFINITY;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, x[k][e]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[k][e] = exp2_hw((x[k][e] - mx) * kLog2e);   // exp2(-inf) = 0 past the row's end
+      sum += x[k][e];
+    }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+  const float inv = 1.f / sum;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int idx = 4 * (lane + 64 * k);
+    if (idx + 3 < n) {
+      const f32x4u_t v = {x[k][0] * inv, x[k][1] * inv, x[k][2] * inv, x[k][3] * inv};
+      *(f32x4u_t*)(p + idx) = v;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (idx + e < n) p[idx + e] = x[k][e] * inv;
+    }
+  }
+}
+
+// --------------------------------------------------------------------------
+// R-SpMM: O[b,h,i,:] = sum_k P[b,h,row_ptr[i] + k] V[b,h,col(i,k),:].  One
+// workgroup per (row group, batch*head).  The V tile goes through LDS (two
+// slots: the next tile's rows are loaded into registers while the current
+// one is multiplied, then written to the other slot; one barrier per tile)
+// so that the V^T operand can be read transposed; the P^T operand comes
+// straight from P in the key order of those reads, split into a bf16 high
+// part and a bf16 remainder (p - hi), each multiplied on the matrix cores:
+// P then enters with about 16 significant bits instead of 8, at the cost of
+// MFMA work this HBM-bound kernel has to spare.
+template <int D, typename OutT>
+__global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
+    const Group* __restrict__ groups, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ row_ptr, const Tile* __restrict__ tiles,
+    const uint64_t* __restrict__ masks, int L, int BH, int64_t nnz, const float* __restrict__ P,
+    const __bf16* __restrict__ V, OutT* __restrict__ O) {
+  constexpr int RB = 2 * D, CPR = RB / 16, TB = kBN * RB, NDB = D / 32;
+  constexpr int CPT = TB / 16 / kTileThreads;   // 16-byte chunks per thread and tile
+  __shared__ __attribute__((aligned(16))) char vt[2][TB];
+
+  const int g = blockIdx.x / BH;
+  const int bh = blockIdx.x - g * BH;
+  const Group grp = groups[g];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int qi = lane & 31, h = lane >> 5;
+  const int m = wave * kWaveRows + qi;
+  const bool row_valid = m < grp.nrows;
+  const int row = row_valid ? rows[grp.row_off + m] : 0;
+  const size_t head = (size_t)bh * L * D;
+  const __bf16* Vh = V + head;
+  const float* prow = P + (size_t)bh * nnz + row_ptr[row];
+
+  int voff[NDB];
+  v_operand_offsets<D>(lane, voff);
+  f32x16_t oacc[NDB];
+#pragma unroll
+  for (int b = 0; b < NDB; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[b][r] = 0.f;
+
+  // chunk c of tile row r is stored at chunk c ^ swz_v(r) of the row
+  auto load_v = [&](const Tile& tl, u32x4_t (&reg)[CPT]) {
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int idx = tid + kTileThreads * k;
+      const int r = idx / CPR, c = idx % CPR;
+      reg[k] = *(const u32x4_t*)(Vh + (size_t)(tl.kb + tl.ks * min(r, tl.nk - 1)) * D + 8 * c);
+    }
+  };
+  auto store_v = [&](char* slot, const u32x4_t (&reg)[CPT]) {
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int idx = tid + kTileThreads * k;
+      const int r = idx / CPR, c = idx % CPR;
+      *(u32x4_t*)(slot + r * RB + 16 * (c ^ swz_v(r))) = reg[k];
+    }
+  };
+
+  const int tb = grp.tile_begin, nt = grp.tile_end - grp.tile_begin;
+  int cnt = 0;
+  if (nt > 0) {
+    u32x4_t vreg[CPT];
+    load_v(tiles[tb], vreg);
+    store_v(vt[0], vreg);
+    __syncthreads();
+    for (int i = 0; i < nt; ++i) {
+      const Tile tl = tiles[tb + i];
+      if (i + 1 < nt) load_v(tiles[tb + i + 1], vreg);
+      const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
+      if (wst != kWaveEmpty) {
+        const uint64_t bits =
+            wst == kWaveFull ? ~0ull : masks[(size_t)max(tl.mask_block, 0) * kBM + m];
+        // P^T operand: k-step j, element e of lane half h is key
+        // u = 16*j + 8*(e/4) + 4*h + e%4
+        float pv[4][8];
+        if (row_valid) {
+          const float* src = prow + cnt;
+          if (wst == kWaveFull) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const f32x4u_t a = *(const f32x4u_t*)(src + 16 * j + 4 * h);
+              const f32x4u_t b = *(const f32x4u_t*)(src + 16 * j + 8 + 4 * h);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                pv[j][e] = a[e];
+                pv[j][4 + e] = b[e];
+              }
+            }
+          } else {
+            // key 8*g + 4*h + e is element 4*(g%2) + e of k-step g/2
+            for_each_key(bits, h, [&](int g, int e, unsigned present, int pos) {
+              pv[g >> 1][4 * (g & 1) + e] = present ? src[pos] : 0.f;
+            });
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pv[j][e] = 0.f;
+        }
+        cnt += popc64(bits);
+        bf16x8_t phi[4], plo[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            phi[j][e] = (__bf16)pv[j][e];
+            plo[j][e] = (__bf16)(pv[j][e] - (float)phi[j][e]);
+          }
+        bf16x8_t va[NDB][4];
+        read_v_operands<D>(lds_addr(vt[i & 1]), voff, va);
+#pragma unroll
+        for (int b = 0; b < NDB; ++b)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            oacc[b] = mfma32(va[b][j], phi[j], oacc[b]);
+            oacc[b] = mfma32(va[b][j], plo[j], oacc[b]);
+          }
+      }
+      if (i + 1 < nt) store_v(vt[(i + 1) & 1], vreg);
+      __syncthreads();
+    }
+  }
+
+  if (row_valid) {
+    OutT* orow = O + head + (size_t)row * D;
+#pragma unroll
+    for (int b = 0; b < NDB; ++b)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg)
+        store4<OutT>(orow + b * 32 + rg * 8 + 4 * h, oacc[b][4 * rg], oacc[b][4 * rg + 1],
+                     oacc[b][4 * rg + 2], oacc[b][4 * rg + 3]);
+  }
+}
+
+template <int NV>
+hipError_t softmax_launch(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {
+  const int64_t n_rows = (int64_t)a.L * BH;
+  const int64_t blocks = (n_rows + 3) / 4;
+  hipLaunchKernelGGL(k_softmax_regs<NV>, dim3((unsigned)blocks), dim3(256), 0, st, a.row_ptr, a.L,
+                     n_rows, a.nnz, S, P);
+  return hipGetLastError();
+}
+
+template <int D, typename OutT>
+hipError_t rspmm_launch(const DevAcsr& a, int BH, const float* P, const void* V, void* O,
+                        hipStream_t st) {
+  hipLaunchKernelGGL((k_rspmm_tiles<D, OutT>), dim3(a.n_groups * BH), dim3(kTileThreads), 0, st,
+                     a.groups, a.rows, a.row_ptr, a.tiles, a.masks, a.L, BH, a.nnz, P,
+                     (const __bf16*)V, (OutT*)O);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_rsddmm_tiles(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
+                               float scale, float* S, hipStream_t st) {
+  if (d == 64)
+    hipLaunchKernelGGL(k_rsddmm_tiles<64>, dim3(a.n_groups * BH), dim3(kTileThreads), 0, st,
+                       a.groups, a.rows, a.row_ptr, a.tiles, a.masks, a.L, BH, a.nnz,
+                       (const __bf16*)Q, (const __bf16*)K, scale, S);
+  else
+    hipLaunchKernelGGL(k_rsddmm_tiles<128>, dim3(a.n_groups * BH), dim3(kTileThreads), 0, st,
+                       a.groups, a.rows, a.row_ptr, a.tiles, a.masks, a.L, BH, a.nnz,
+                       (const __bf16*)Q, (const __bf16*)K, scale, S);
+  return hipGetLastError();
+}
+
+bool softmax_regs_fits(const DevAcsr& a) { return a.max_row_nnz <= 256 * 16; }
+
+hipError_t launch_softmax_regs(const DevAcsr& a, int BH, const float* S, float* P,
+                               hipStream_t st) {
+  const int n = a.max_row_nnz;
+  if (n <= 256) return softmax_launch<1>(a, BH, S, P, st);
+  if (n <= 512) return softmax_launch<2>(a, BH, S, P, st);
+  if (n <= 1024) return softmax_launch<4>(a, BH, S, P, st);
+  if (n <= 2048) return softmax_launch<8>(a, BH, S, P, st);
+  return softmax_launch<16>(a, BH, S, P, st);
+}
+
+hipError_t launch_rspmm_tiles(const DevAcsr& a, int BH, int d, const float* P, const void* V,
+                              void* O, int out_dtype, hipStream_t st) {
+  if (d == 64)
+    return out_dtype == 0 ? rspmm_launch<64, float>(a, BH, P, V, O, st)
+                          : rspmm_launch<64, __bf16>(a, BH, P, V, O, st);
+  return out_dtype == 0 ? rspmm_launch<128, float>(a, BH, P, V, O, st)
+                        : rspmm_launch<128, __bf16>(a, BH, P, V, O, st);
+}
+
+}  // namespace splat

@@ -12,6 +12,7 @@ namespace splat {
 struct DevAcsr {
   int32_t L;
   int64_t nnz;
+  int32_t max_row_nnz;
   int32_t n_groups;
   const int32_t* row_ptr;   // L + 1
   const RowRuns* runs;      // L
@@ -35,6 +36,15 @@ hipError_t launch_fused_rows(const DevAcsr& a, int dtype, int BH, int d, const v
                              hipStream_t st);
 
 // Matrix-core kernels over the tile plan: bf16 inputs, d in {64, 128}.
+hipError_t launch_rsddmm_tiles(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
+                               float scale, float* S, hipStream_t st);
+hipError_t launch_rspmm_tiles(const DevAcsr& a, int BH, int d, const float* P, const void* V,
+                              void* O, int out_dtype, hipStream_t st);
+
+// Row softmax with each row held in registers: rows of at most 4096 values.
+bool softmax_regs_fits(const DevAcsr& a);
+hipError_t launch_softmax_regs(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st);
+
 hipError_t launch_fused_mfma(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
                              const void* V, float scale, void* O, int out_dtype, hipStream_t st);
 

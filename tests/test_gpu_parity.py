@@ -96,8 +96,10 @@ def test_small_configs_full_oracle(gpu_lib, cfg):
         errs[f"fused/{odt}"] = check_O(O, ref, w.dtype if odt == torch.float32 else "bf16",
                                        f"cfg{cfg} fused out={odt}")
     S, P, O = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    O16 = splat.rspmm(a, P, Vd, out_dtype=torch.bfloat16)
     torch.cuda.synchronize()
     errs["unfused"] = check_O(O, ref, w.dtype, f"cfg{cfg} unfused")
+    errs["unfused/bf16"] = check_O(O16, ref, "bf16", f"cfg{cfg} unfused out=bf16")
     S, P = S.cpu().numpy(), P.cpu().numpy()
     for b in range(w.B):
         for h in range(w.H):
@@ -170,6 +172,8 @@ EDGE = [
     ("full", {}, 1, 64),
     ("full", {}, 200, 64),
     ("window", {"w": 700}, 513, 128),
+    # rows longer than 4096 values: the softmax takes its streaming path
+    ("window", {"w": 2100}, 4300, 64),
 ]
 
 
