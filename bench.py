@@ -29,25 +29,28 @@ PEAK_HBM_GBS = 8000.0
 
 
 def kernel_source_sha() -> str:
+    """Hash of every native source: counter figures taken on other sources are stale."""
     h = hashlib.sha256()
-    for f in ("kernels_mfma.hip", "acsr_core.hpp", "acsr_host.cpp"):
-        with open(os.path.join(ROOT, "paper_2407_16847_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    csrc = os.path.join(ROOT, "paper_2407_16847_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload: str):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they
-    were taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"traffic_fused_{workload}.json")
+def load_traffic(workload: str) -> dict:
+    """HBM bytes per launch of each kernel ("fused", "rsddmm", "row_softmax",
+    "rspmm") from the committed rocprofv3 counter runs, if they were taken on
+    the current sources; empty otherwise."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     try:
         with open(path) as f:
             t = json.load(f)
     except (OSError, ValueError):
-        return None
+        return {}
     if t.get("source_sha") != kernel_source_sha():
-        return None
-    return t.get("traffic_bytes")
+        return {}
+    return {k: v.get("traffic_bytes") for k, v in t.get("kernels", {}).items()}
 
 
 def cpu_baseline(w, Q, K, V, budget_s: float):
@@ -140,6 +143,8 @@ def main() -> int:
     in_bytes = 3 * w.B * w.H * w.L * w.d * Qd.element_size()
     out_bytes = w.B * w.H * w.L * w.d * O.element_size()
 
+    traffic = load_traffic(w.name)
+
     # unfused chain (SDDMM -> softmax -> SpMM), per kernel
     unfused = None
     if not args.no_unfused:
@@ -167,12 +172,15 @@ def main() -> int:
         E = w.B * w.H * nnz
         dense_e = w.B * w.H * w.L * w.d * Qd.element_size()
         t = [x / n_rep for x in tot]
-        unfused = {
-            "rsddmm_ms": t[0], "row_softmax_ms": t[1], "rspmm_ms": t[2], "total_ms": sum(t),
-            "rsddmm_GBps": (2 * dense_e + 4 * E) / (t[0] * 1e-3) / 1e9,
-            "row_softmax_GBps": (8 * E) / (t[1] * 1e-3) / 1e9,
-            "rspmm_GBps": (4 * E + dense_e + w.B * w.H * w.L * w.d * Ou.element_size()) / (t[2] * 1e-3) / 1e9,
-        }
+        # algorithmic bytes per launch: inputs read once, outputs written once
+        alg = {"rsddmm": 2 * dense_e + 4 * E, "row_softmax": 8 * E,
+               "rspmm": 4 * E + dense_e + w.B * w.H * w.L * w.d * Ou.element_size()}
+        unfused = {"total_ms": round(sum(t), 4), "bound": "hbm", "peak_GBps": PEAK_HBM_GBS}
+        for k, name in enumerate(("rsddmm", "row_softmax", "rspmm")):
+            gbs = alg[name] / (t[k] * 1e-3) / 1e9
+            unfused[name] = {"ms": round(t[k], 4), "algorithmic_bytes": alg[name],
+                             "GBps": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4),
+                             "traffic": traffic.get(name)}
         del S, P, Ou
 
     if args.copy_calibration:
@@ -186,7 +194,6 @@ def main() -> int:
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, Q, K, V, args.cpu_seconds)
 
-    traffic = load_traffic(w.name)
     line = {
         "metric": "sparse-MHSA fwd effective TFLOP/s on nnz (% of bf16 MFMA peak), L=4096",
         "value": round(tflops, 2),
@@ -207,8 +214,9 @@ def main() -> int:
                    "path": "fused"},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic,
-                     "kernel": "k_fused_mfma<64, bf16>",
+                     "traffic": traffic.get("fused"),
+                     "kernel": (f"k_fused_mfma<{w.d}, {args.out_dtype}>" if w.dtype == "bf16"
+                                else "k_fused_rows"),
                      "algorithmic_flops_per_launch": flops,
                      "min_hbm_bytes_per_launch": in_bytes + out_bytes,
                      "tile_efficiency": round(nnz / info["computed"], 4)},
