@@ -5,10 +5,12 @@
 // 4 wavefronts x 32 query rows.  For every planned key tile of its group:
 //
 //   1. K and V tiles [64 keys][d] and the rows' tile masks travel from global
-//      memory straight into a ring of LDS slots (global_load_lds, no staging
-//      registers), issued NSLOT-1 tiles ahead; rows are stored unpadded with
-//      their 16-byte chunks XOR-swizzled so the MFMA operand reads below are
-//      free of bank conflicts
+//      memory straight into a two-slot LDS ring (global_load_lds from a scalar
+//      tile base plus per-lane offsets, no staging registers), the next tile
+//      issued while this one is computed; rows are stored unpadded with their
+//      16-byte chunks XOR-swizzled so the MFMA operand reads below are free of
+//      bank conflicts.  With 34 KiB of LDS and at most 128 VGPRs (d = 64),
+//      four workgroups share a CU: four wavefronts per SIMD to hide latency
 //   2. S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q^T stays in registers); in this
 //      orientation each lane holds 32 scores of ONE query, so the row max and
 //      row sum need one exchange with lane ^ 32 only
@@ -19,8 +21,9 @@
 //      the running max m is only raised when a score exceeds it by more
 //      than 2^8 (so p <= 256 and O is rescaled rarely)
 //   5. O^T += V^T P^T on the same MFMA, P^T taken straight from the score
-//      registers (rounded to bf16), V^T gathered by LDS transpose reads in
-//      the key order the score registers imply
+//      registers (rounded toward zero to bf16 by one v_perm_b32 per pair; the
+//      row sum adds the same rounded values), V^T gathered by LDS transpose
+//      reads in the key order the score registers imply
 //
 // At the end O = O^T / (row sum), written in the requested dtype.
 #include <hip/hip_runtime.h>
@@ -45,7 +48,7 @@ struct Geo {
   static constexpr int NBW = TB / kDmaBlock / 4;        // loads per wavefront per tile
   static constexpr int RPB = kDmaBlock / RB;            // rows per load
   static constexpr int SLOT = 2 * TB + kBM * 8;         // K tile, V tile, row masks
-  static constexpr int NSLOT = D == 64 ? 3 : 2;         // ring depth
+  static constexpr int NSLOT = 2;                       // ring depth
   static constexpr int OPS = 2 * NBW + 1;               // vector-memory ops per wavefront per tile
   static constexpr int LDS = NSLOT * SLOT;
   static constexpr int NKS = D / 16, NDB = D / 32;
@@ -61,25 +64,53 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
                                            int lane) {
   using G = Geo<D>;
   const int last = tl.nk - 1;
+  // uniform tile bases (scalar registers) + 32-bit per-lane byte offsets
+  const char* kbase = (const char*)(Kh + (size_t)tl.kb * D);
+  const char* vbase = (const char*)(Vh + (size_t)tl.kb * D);
 #pragma unroll
   for (int k = 0; k < G::NBW; ++k) {
     const int bk = wave + 4 * k;
     const int r = bk * G::RPB + lane / G::CPR;
     const int pos = lane % G::CPR;
-    const size_t row = (size_t)(tl.kb + tl.ks * min(r, last)) * D;
-    dma16(Kh + row + 8 * (pos ^ swz_k(r)), slot + bk * kDmaBlock);
-    dma16(Vh + row + 8 * (pos ^ swz_v(r)), slot + G::TB + bk * kDmaBlock);
+    const unsigned row = (unsigned)(tl.ks * min(r, last)) * (2u * D);
+    dma16(kbase + row + 16u * (pos ^ swz_k(r)), slot + bk * kDmaBlock);
+    dma16(vbase + row + 16u * (pos ^ swz_v(r)), slot + G::TB + bk * kDmaBlock);
   }
   const uint64_t* mrow = masks + (size_t)max(tl.mask_block, 0) * kBM + wave * 32 + 2 * lane;
   if (lane < 16) dma16(mrow, slot + 2 * G::TB + wave * 256);
 }
 
+// p = exp2(s * sl2 - m) for this lane's 32 scores, rounded toward zero to bf16
+// into the P^T operand (key order of the score registers); returns the sum
+// of the rounded values.
+__device__ __forceinline__ float tile_exp(const f32x16_t* s, float sl2, float neg_m,
+                                          bf16x8_t* pf) {
+  float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float e8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) e8[e] = exp2_hw(fmaf(s[j >> 1][(j & 1) * 8 + e], sl2, neg_m));
+    bf16x2_t p2[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) p2[e] = pack_bf16_rz(e8[2 * e], e8[2 * e + 1]);
+    pf[j] = __builtin_shufflevector(__builtin_shufflevector(p2[0], p2[1], 0, 1, 2, 3),
+                                    __builtin_shufflevector(p2[2], p2[3], 0, 1, 2, 3), 0, 1, 2, 3,
+                                    4, 5, 6, 7);
+    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[0], kOnes2, l0, false);
+    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[1], kOnes2, l1, false);
+    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[2], kOnes2, l0, false);
+    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[3], kOnes2, l1, false);
+  }
+  return l0 + l1;
+}
+
 // Online-softmax step of one tile for this lane's row: optional mask, tile
 // max, lazy update of the running max (only when a score exceeds it by more
-// than 2^kRescaleThreshold), p = exp2(s * scale*log2(e) - m) rounded to bf16
-// into the P^T operand, running sum of the rounded p.  alpha is the factor the
-// output accumulator must be scaled by before this tile's P V is added;
-// the return value says whether any lane of the wavefront needs it.
+// than 2^kRescaleThreshold), p = exp2(s * scale*log2(e) - m) into the P^T
+// operand and the running sum of the rounded p.  alpha is the factor the
+// output accumulator must be scaled by before this tile's P V is added; the
+// return value says whether any lane of the wavefront needs it.
 template <bool MASKED>
 __device__ __forceinline__ bool tile_softmax(f32x16_t* s, uint64_t mk, int h, float sl2,
                                              float& m_run, float& l_run, float& alpha,
@@ -87,12 +118,11 @@ __device__ __forceinline__ bool tile_softmax(f32x16_t* s, uint64_t mk, int h, fl
   if (MASKED) {
     const uint64_t bits = mk >> (4 * h);
 #pragma unroll
-    for (int kb2 = 0; kb2 < 2; ++kb2)
+    for (int kb2 = 0; kb2 < 2; ++kb2) {
+      const unsigned word = (unsigned)(bits >> (32 * kb2));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int u = 32 * kb2 + 8 * (r >> 2) + (r & 3);
-        if (!((bits >> u) & 1ull)) s[kb2][r] = -INFINITY;
-      }
+      for (int r = 0; r < 16; ++r) s[kb2][r] = keep_if_bit(s[kb2][r], word, 8 * (r >> 2) + (r & 3));
+    }
   }
   float mx0 = -INFINITY, mx1 = -INFINITY;
 #pragma unroll
@@ -108,22 +138,7 @@ __device__ __forceinline__ bool tile_softmax(f32x16_t* s, uint64_t mk, int h, fl
   m_run = need ? m_new : m_run;
   l_run *= alpha;
   const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
-  float l0 = 0.f, l1 = 0.f;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      pf[j][e] = (__bf16)exp2_hw(fmaf(s[j >> 1][(j & 1) * 8 + e], sl2, neg_m));
-    // row sum of the bf16-rounded p, two at a time, two partial sums
-#pragma unroll
-    for (int e = 0; e < 8; e += 4) {
-      const bf16x2_t p0 = {pf[j][e], pf[j][e + 1]};
-      const bf16x2_t p1 = {pf[j][e + 2], pf[j][e + 3]};
-      l0 = __builtin_amdgcn_fdot2_f32_bf16(p0, kOnes2, l0, false);
-      l1 = __builtin_amdgcn_fdot2_f32_bf16(p1, kOnes2, l1, false);
-    }
-  }
-  l_run += l0 + l1;
+  l_run += tile_exp(s, sl2, neg_m, pf);
   return __any(need);
 }
 
@@ -131,7 +146,7 @@ __device__ __forceinline__ bool tile_softmax(f32x16_t* s, uint64_t mk, int h, fl
 // so their (wavefront-uniform) reads are scalar loads, independent of the
 // vector-memory counter that tracks the global->LDS loads.
 template <int D, typename OutT>
-__global__ __launch_bounds__(kThreads, D == 64 ? 3 : 2) void k_fused_mfma(
+__global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
     const Group* __restrict__ groups, const int32_t* __restrict__ rows,
     const Tile* __restrict__ tiles, const uint64_t* __restrict__ masks, int L, int BH,
     const __bf16* __restrict__ Q, const __bf16* K, const __bf16* V, float sl2,
@@ -207,20 +222,23 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 3 : 2) void k_fused_mfma(
         const __bf16* cK = (const __bf16*)cur;
         const __bf16* cV = (const __bf16*)(cur + G::TB);
         // S^T[key][query]: all K operands read, then the products
-        bf16x8_t ka[2][NKS];
+        auto scores = [&](f32x16_t* sacc) {
+          bf16x8_t ka[2][NKS];
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
+          for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-          for (int ks = 0; ks < NKS; ++ks)
-            ka[kb2][ks] = *(const bf16x8_t*)((const char*)cK + kb2 * 32 * RB + koff[ks]);
+            for (int ks = 0; ks < NKS; ++ks)
+              ka[kb2][ks] = *(const bf16x8_t*)((const char*)cK + kb2 * 32 * RB + koff[ks]);
+#pragma unroll
+          for (int kb2 = 0; kb2 < 2; ++kb2) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sacc[kb2][r] = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) sacc[kb2] = mfma32(ka[kb2][ks], qf[ks], sacc[kb2]);
+          }
+        };
         f32x16_t sacc[2];
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sacc[kb2][r] = 0.f;
-#pragma unroll
-          for (int ks = 0; ks < NKS; ++ks) sacc[kb2] = mfma32(ka[kb2][ks], qf[ks], sacc[kb2]);
-        }
+        scores(sacc);
         float alpha;
         bf16x8_t pf[4];
         bool need;

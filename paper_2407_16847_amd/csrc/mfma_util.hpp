@@ -52,6 +52,14 @@ __device__ __forceinline__ bf16x4_t tr16_async(unsigned lds_addr) {
   asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(lds_addr));
   return __builtin_bit_cast(bf16x4_t, v);
 }
+// ... with a constant byte offset folded into the instruction (no address add)
+template <int OFF>
+__device__ __forceinline__ bf16x4_t tr16_async_at(unsigned lds_addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  i16x4_t v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(lds_addr), "i"(OFF));
+  return __builtin_bit_cast(bf16x4_t, v);
+}
 
 // Wait for every outstanding LDS read of this wavefront; the operands make the
 // values read by tr16_async depend on the wait.
@@ -101,14 +109,18 @@ __device__ __forceinline__ void dma16(const void* g, char* lds) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, kDmaBytes, 0, 0);
 }
 
-// Wait until at most `pending` vector-memory ops of this wavefront are
-// outstanding and all of its LDS reads are done, then barrier.  The empty asm
-// statements keep the compiler from moving LDS accesses across it.
+// Wait until at most `pending` vector-memory ops (the global->LDS loads) of
+// this wavefront are outstanding, then barrier.  The LDS/scalar counter is
+// left alone: every LDS read before a ring barrier has its result consumed
+// by then (the compiler waits before the first use, lds_wait() covers the
+// transpose reads), and waiting on it here would also wait for the scalar
+// loads of upcoming tile descriptors.  The empty asm statements keep the
+// compiler from moving LDS accesses across the barrier.
 template <int PENDING>
 __device__ __forceinline__ void ring_sync() {
   static_assert(PENDING < 64, "vmcnt field");
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt((PENDING & 15) | ((PENDING >> 4) << 14) | (7 << 4));
+  __builtin_amdgcn_s_waitcnt((PENDING & 15) | ((PENDING >> 4) << 14) | (7 << 4) | (15 << 8));
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -128,19 +140,36 @@ __device__ __forceinline__ void v_operand_offsets(int lane, int (&voff)[D / 32])
   for (int b = 0; b < D / 32; ++b) voff[b] = rv * RB + 16 * ((4 * b + cl) ^ swz_v(rv)) + 8 * (i & 1);
 }
 
+template <int D, int J = 0>
+__device__ __forceinline__ void read_v_block(unsigned vp, bf16x8_t (&vb)[4]) {
+  constexpr int RB = 2 * D;
+  if constexpr (J < 4) {
+    vb[J] = __builtin_shufflevector(tr16_async_at<16 * J * RB>(vp),
+                                    tr16_async_at<16 * J * RB + 8 * RB>(vp), 0, 1, 2, 3, 4, 5, 6, 7);
+    read_v_block<D, J + 1>(vp, vb);
+  }
+}
+
 template <int D>
 __device__ __forceinline__ void read_v_operands(unsigned vbase, const int (&voff)[D / 32],
                                                 bf16x8_t (*va)[4]) {
-  constexpr int RB = 2 * D;
 #pragma unroll
-  for (int b = 0; b < D / 32; ++b)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const unsigned vp = vbase + voff[b] + 16 * j * RB;
-      va[b][j] = __builtin_shufflevector(tr16_async(vp), tr16_async(vp + 8 * RB), 0, 1, 2, 3, 4,
-                                         5, 6, 7);
-    }
+  for (int b = 0; b < D / 32; ++b) read_v_block<D>(vbase + voff[b], va[b]);
   lds_wait<D / 32>(va);
+}
+
+// Two fp32 values to a bf16 pair by dropping their low 16 bits (rounding
+// toward zero): one full-rate v_perm_b32 instead of a half-rate conversion.
+__device__ __forceinline__ bf16x2_t pack_bf16_rz(float lo, float hi) {
+  const unsigned r = __builtin_amdgcn_perm(__builtin_bit_cast(unsigned, hi),
+                                           __builtin_bit_cast(unsigned, lo), 0x07060302u);
+  return __builtin_bit_cast(bf16x2_t, r);
+}
+
+// x where bit u of `word` is set, -inf elsewhere (v_bfe_i32 + v_bfi_b32)
+__device__ __forceinline__ float keep_if_bit(float x, unsigned word, int u) {
+  const unsigned m = (unsigned)__builtin_amdgcn_sbfe((int)word, u, 1);
+  return __builtin_bit_cast(float, (__builtin_bit_cast(unsigned, x) & m) | (0xff800000u & ~m));
 }
 
 }  // namespace mfma
