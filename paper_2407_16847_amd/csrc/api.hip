@@ -333,9 +333,7 @@ splat_status splat_row_softmax(splat_acsr_t h, int32_t B, int32_t H, const float
   if (s0 != p0 && s0 < p0 + bytes && p0 < s0 + bytes)
     return fail(SPLAT_ERR_INVALID_ARG, "S and P overlap without being equal");
   hipStream_t st = (hipStream_t)stream;
-  if (splat::softmax_regs_fits(h->dev))
-    return launched(splat::launch_softmax_regs(h->dev, B * H, S, P, st), "row_softmax");
-  return launched(splat::launch_softmax_rows(h->dev, B * H, S, P, st), "row_softmax");
+  return launched(splat::launch_softmax(h->dev, B * H, S, P, st), "row_softmax");
 }
 
 splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,

@@ -4,7 +4,7 @@
 // 5.1: the k-th value of run r sits at column start + stride * k) and serve
 // every dtype and pattern: they are the fp32 path (fp32 FMA throughout, the
 // library's accurate path) and run any request the matrix-core kernels do
-// not take.  Lanes own keys (SDDMM, softmax) or output features (SpMM).
+// not take.  Lanes own keys (SDDMM, fused) or output features (SpMM).
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -74,22 +74,6 @@ __global__ __launch_bounds__(kWave) void k_rsddmm_rows(DevAcsr a, int d, const T
       out[q.prefix + k] = dot_row(qs, K + head + (size_t)j * d, d) * scale;
     }
   }
-}
-
-__global__ __launch_bounds__(kWave) void k_softmax_rows(DevAcsr a, const float* S, float* P) {
-  const int i = blockIdx.x, bh = blockIdx.y, lane = threadIdx.x;
-  const int n = a.row_ptr[i + 1] - a.row_ptr[i];
-  if (n == 0) return;
-  const size_t base = (size_t)bh * a.nnz + a.row_ptr[i];
-  float m = -INFINITY;
-  for (int k = lane; k < n; k += kWave) m = fmaxf(m, S[base + k]);
-  m = wave_max(m);
-  float l = 0.f;
-  for (int k = lane; k < n; k += kWave) l += expf(S[base + k] - m);
-  l = wave_sum(l);
-  const float inv = 1.f / l;
-  // each element is read and then written by the same lane: P may alias S
-  for (int k = lane; k < n; k += kWave) P[base + k] = expf(S[base + k] - m) * inv;
 }
 
 template <typename T, typename OutT>
@@ -181,11 +165,6 @@ hipError_t launch_rsddmm_rows(const DevAcsr& a, int dtype, int BH, int d, const 
   else
     hipLaunchKernelGGL(k_rsddmm_rows<__bf16>, grid, dim3(kWave), 0, st, a, d, (const __bf16*)Q,
                        (const __bf16*)K, scale, S);
-  return hipGetLastError();
-}
-
-hipError_t launch_softmax_rows(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {
-  hipLaunchKernelGGL(k_softmax_rows, dim3(a.L, BH), dim3(kWave), 0, st, a, S, P);
   return hipGetLastError();
 }
 

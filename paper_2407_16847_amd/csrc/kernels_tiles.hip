@@ -25,6 +25,7 @@ namespace {
 using namespace mfma;
 
 constexpr int kTileThreads = 256;   // 4 wavefronts x 32 rows of a group
+constexpr int kStageStride = 68;    // floats per staged score row: 64 + 4 against bank conflicts
 
 // 4 floats at a 4-byte aligned address (values of a row start anywhere)
 typedef float f32x4u_t __attribute__((ext_vector_type(4), aligned(4)));
@@ -58,7 +59,10 @@ __device__ __forceinline__ void for_each_key(uint64_t bits, int h, F&& f) {
 // read straight from global memory (16 bytes per lane; the 4 wavefronts of a
 // group read the same K tile, which stays in cache), then stores the scores
 // of the row's columns.  Lane (qi, h) holds keys 32*kb2 + 8*(r/4) + 4*h + r%4
-// of query row qi, so on FULL tiles it writes 4 consecutive values at a time.
+// of query row qi.  On FULL tiles the 32 x 64 scores go through a per-
+// wavefront LDS buffer and come back as row segments, so each store writes
+// 4 rows x 256 contiguous bytes (16 lanes per row) instead of 32 rows x 32
+// bytes; on PARTIAL tiles each present score is stored at its rank.
 template <int D>
 __global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
     const Group* __restrict__ groups, const int32_t* __restrict__ rows,
@@ -92,21 +96,27 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
       }
     }
   }
-  float* srow = S + (size_t)bh * nnz + row_ptr[row];
+  float* const Sh = S + (size_t)bh * nnz;
+  const int roff = row_valid ? row_ptr[row] : 0;
+  float* srow = Sh + roff;
   int cnt = 0;
+  __shared__ __attribute__((aligned(16))) float stage[kTileThreads / 64][kWaveRows * kStageStride];
+  float* const stw = stage[wave];
 
-  for (int t = grp.tile_begin; t < grp.tile_end; ++t) {
-    const Tile tl = tiles[t];
-    const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
-    if (wst == kWaveEmpty) continue;
+  // K operands of a tile (keys past its end re-read the last key)
+  auto load_k = [&](const Tile& tl, bf16x8_t (&ka)[2][NKS]) {
     const int last = tl.nk - 1;
-    bf16x8_t ka[2][NKS];
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2) {
       const __bf16* krow = Kh + (size_t)(tl.kb + tl.ks * min(32 * kb2 + qi, last)) * D + 8 * h;
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) ka[kb2][ks] = *(const bf16x8_t*)(krow + 16 * ks);
     }
+  };
+  // One tile: this wavefront's scores of the tile, stored at their ranks.
+  auto tile = [&](const Tile& tl, const bf16x8_t (&ka)[2][NKS]) {
+    const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
+    if (wst == kWaveEmpty) return;
     const uint64_t bits =
         wst == kWaveFull ? ~0ull : masks[(size_t)max(tl.mask_block, 0) * kBM + m];
     f32x16_t sacc[2];
@@ -117,18 +127,31 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) sacc[kb2] = mfma32(ka[kb2][ks], qf[ks], sacc[kb2]);
     }
-    if (row_valid) {
+    if (wst == kWaveFull) {
+      // scores into the staging rows, then out as row segments
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const float4 v = make_float4(sacc[kb2][4 * rg] * scale, sacc[kb2][4 * rg + 1] * scale,
+                                       sacc[kb2][4 * rg + 2] * scale, sacc[kb2][4 * rg + 3] * scale);
+          *(float4*)(stw + qi * kStageStride + 32 * kb2 + 8 * rg + 4 * h) = v;
+        }
+      const int my_off = row_valid ? roff + cnt : -1;   // this row's values of the tile
+      const int rr = lane >> 4, cc = lane & 15;
+#pragma unroll
+      for (int it = 0; it < kWaveRows / 4; ++it) {
+        const int r = 4 * it + rr;
+        const float4 v = *(const float4*)(stw + r * kStageStride + 4 * cc);
+        const int off = __shfl(my_off, r, 64);
+        if (off >= 0) {
+          const f32x4u_t o = {v.x, v.y, v.z, v.w};
+          *(f32x4u_t*)(Sh + off + 4 * cc) = o;
+        }
+      }
+    } else if (row_valid) {
       float* dst = srow + cnt;
-      if (wst == kWaveFull) {
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-          for (int rg = 0; rg < 4; ++rg) {
-            const f32x4u_t v = {sacc[kb2][4 * rg] * scale, sacc[kb2][4 * rg + 1] * scale,
-                                sacc[kb2][4 * rg + 2] * scale, sacc[kb2][4 * rg + 3] * scale};
-            *(f32x4u_t*)(dst + 32 * kb2 + 8 * rg + 4 * h) = v;
-          }
-      } else {
+      {
         // key 8*g + 4*h + e is element 4*(g%4) + e of sacc[g/4]
         for_each_key(bits, h, [&](int g, int e, unsigned present, int pos) {
           if (present) dst[pos] = sacc[g >> 2][4 * (g & 3) + e] * scale;
@@ -136,19 +159,78 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
       }
     }
     cnt += popc64(bits);
+  };
+  // The next tile's K operands are loaded before this tile's scores are
+  // stored, so waiting for them never waits for the stores (which share the
+  // vector-memory counter); two operand buffers alternate, so no copies.
+  const int tb = grp.tile_begin, te = grp.tile_end;
+  if (tb >= te) return;
+  bf16x8_t kA[2][NKS], kB[2][NKS];
+  Tile tA = tiles[tb];
+  load_k(tA, kA);
+  int t = tb;
+  for (; t + 1 < te; t += 2) {
+    const Tile tB = tiles[t + 1];
+    load_k(tB, kB);
+    tile(tA, kA);
+    tA = tiles[min(t + 2, te - 1)];
+    load_k(tA, kA);
+    tile(tB, kB);
   }
+  if (t < te) tile(tA, kA);
 }
 
 // --------------------------------------------------------------------------
 // Row softmax over the non-zeros (section 6): one wavefront per (batch*head,
-// row), the row's values held in registers (4 consecutive values per lane
-// and load, NV loads), so S is read once and P written once.  P may alias S:
-// every value is read before any is written, each by the lane that writes it.
-template <int NV>
-__global__ __launch_bounds__(256) void k_softmax_regs(const int32_t* __restrict__ row_ptr, int L,
-                                                      int64_t n_rows, int64_t nnz, const float* S,
-                                                      float* P) {
+// row).  A row of at most 256 * NV values is held in registers (4 consecutive
+// values per lane and load), so S is read once and P written once; a longer
+// row is streamed twice, first for its maximum and sum (a running maximum per
+// lane, the sum rescaled when it grows), then to write P.  P may alias S:
+// every value is read before it is written, by the lane that writes it.
+// NV is kept small (registers bound how many wavefronts keep loads in flight)
+// since rows far longer than the typical one are rare.
+__device__ __forceinline__ float ex2_from(float x, float m) {
   constexpr float kLog2e = 1.4426950408889634f;
+  return x == -INFINITY ? 0.f : exp2_hw((x - m) * kLog2e);
+}
+
+__device__ __forceinline__ void load4_row(const float* s, int idx, int n, float (&x)[4]) {
+  if (idx + 3 < n) {
+    const f32x4u_t v = *(const f32x4u_t*)(s + idx);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = v[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = idx + e < n ? s[idx + e] : -INFINITY;
+  }
+}
+
+__device__ __forceinline__ void store4_row(float* p, int idx, int n, const float (&y)[4]) {
+  if (idx + 3 < n) {
+    const f32x4u_t v = {y[0], y[1], y[2], y[3]};
+    *(f32x4u_t*)(p + idx) = v;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (idx + e < n) p[idx + e] = y[e];
+  }
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+template <int NV>
+__global__ __launch_bounds__(256) void k_softmax(const int32_t* __restrict__ row_ptr, int L,
+                                                 int64_t n_rows, int64_t nnz, const float* S,
+                                                 float* P) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * 4 + wave;
   if (r >= n_rows) return;
@@ -161,46 +243,54 @@ __global__ __launch_bounds__(256) void k_softmax_regs(const int32_t* __restrict_
   const float* s = S + base;
   float* p = P + base;
 
-  float x[NV][4];
-  float mx = -INFINITY;
+  if (n <= 256 * NV) {
+    float x[NV][4];
+    float mx = -INFINITY;
 #pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    const int idx = 4 * (lane + 64 * k);
-    if (idx + 3 < n) {
-      const f32x4u_t v = *(const f32x4u_t*)(s + idx);
+    for (int k = 0; k < NV; ++k) {
+      load4_row(s, 4 * (lane + 64 * k), n, x[k]);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[k][e] = v[e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x[k][e] = idx + e < n ? s[idx + e] : -INFINITY;
+      for (int e = 0; e < 4; ++e) mx = fmaxf(mx, x[k][e]);
     }
+    mx = wave_max(mx);
+    float sum = 0.f;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, x[k][e]);
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[k][e] = ex2_from(x[k][e], mx);
+        sum += x[k][e];
+      }
+    const float inv = 1.f / wave_sum(sum);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[k][e] *= inv;
+      store4_row(p, 4 * (lane + 64 * k), n, x[k]);
+    }
+    return;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-  float sum = 0.f;
-#pragma unroll
-  for (int k = 0; k < NV; ++k)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[k][e] = exp2_hw((x[k][e] - mx) * kLog2e);   // exp2(-inf) = 0 past the row's end
-      sum += x[k][e];
+  // long row: running maximum and rescaled sum per lane, then the write pass
+  float mx = -INFINITY, sum = 0.f;
+  for (int c0 = 0; c0 < n; c0 += 256) {
+    float x[4];
+    load4_row(s, c0 + 4 * lane, n, x);
+    const float cm = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    if (cm > mx) {
+      sum *= ex2_from(mx, cm);
+      mx = cm;
     }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
-  const float inv = 1.f / sum;
+    for (int e = 0; e < 4; ++e) sum += ex2_from(x[e], mx);
+  }
+  const float gm = wave_max(mx);
+  const float inv = 1.f / wave_sum(sum * ex2_from(mx, gm));
+  for (int c0 = 0; c0 < n; c0 += 256) {
+    float x[4];
+    load4_row(s, c0 + 4 * lane, n, x);
 #pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    const int idx = 4 * (lane + 64 * k);
-    if (idx + 3 < n) {
-      const f32x4u_t v = {x[k][0] * inv, x[k][1] * inv, x[k][2] * inv, x[k][3] * inv};
-      *(f32x4u_t*)(p + idx) = v;
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (idx + e < n) p[idx + e] = x[k][e] * inv;
-    }
+    for (int e = 0; e < 4; ++e) x[e] = ex2_from(x[e], gm) * inv;
+    store4_row(p, c0 + 4 * lane, n, x);
   }
 }
 
@@ -344,7 +434,7 @@ template <int NV>
 hipError_t softmax_launch(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {
   const int64_t n_rows = (int64_t)a.L * BH;
   const int64_t blocks = (n_rows + 3) / 4;
-  hipLaunchKernelGGL(k_softmax_regs<NV>, dim3((unsigned)blocks), dim3(256), 0, st, a.row_ptr, a.L,
+  hipLaunchKernelGGL(k_softmax<NV>, dim3((unsigned)blocks), dim3(256), 0, st, a.row_ptr, a.L,
                      n_rows, a.nnz, S, P);
   return hipGetLastError();
 }
@@ -373,16 +463,12 @@ hipError_t launch_rsddmm_tiles(const DevAcsr& a, int BH, int d, const void* Q, c
   return hipGetLastError();
 }
 
-bool softmax_regs_fits(const DevAcsr& a) { return a.max_row_nnz <= 256 * 16; }
-
-hipError_t launch_softmax_regs(const DevAcsr& a, int BH, const float* S, float* P,
-                               hipStream_t st) {
+hipError_t launch_softmax(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {
   const int n = a.max_row_nnz;
   if (n <= 256) return softmax_launch<1>(a, BH, S, P, st);
   if (n <= 512) return softmax_launch<2>(a, BH, S, P, st);
   if (n <= 1024) return softmax_launch<4>(a, BH, S, P, st);
-  if (n <= 2048) return softmax_launch<8>(a, BH, S, P, st);
-  return softmax_launch<16>(a, BH, S, P, st);
+  return softmax_launch<8>(a, BH, S, P, st);   // longer rows take the two-pass path
 }
 
 hipError_t launch_rspmm_tiles(const DevAcsr& a, int BH, int d, const float* P, const void* V,

@@ -28,7 +28,6 @@ struct DevAcsr {
 // Row-per-wave kernels: any d in {64, 128}, both dtypes.
 hipError_t launch_rsddmm_rows(const DevAcsr& a, int dtype, int BH, int d, const void* Q,
                               const void* K, float scale, float* S, hipStream_t st);
-hipError_t launch_softmax_rows(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st);
 hipError_t launch_rspmm_rows(const DevAcsr& a, int dtype, int BH, int d, const float* P,
                              const void* V, void* O, int out_dtype, hipStream_t st);
 hipError_t launch_fused_rows(const DevAcsr& a, int dtype, int BH, int d, const void* Q,
@@ -41,9 +40,8 @@ hipError_t launch_rsddmm_tiles(const DevAcsr& a, int BH, int d, const void* Q, c
 hipError_t launch_rspmm_tiles(const DevAcsr& a, int BH, int d, const float* P, const void* V,
                               void* O, int out_dtype, hipStream_t st);
 
-// Row softmax with each row held in registers: rows of at most 4096 values.
-bool softmax_regs_fits(const DevAcsr& a);
-hipError_t launch_softmax_regs(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st);
+// Row softmax, any row length (rows of up to 2048 values in registers).
+hipError_t launch_softmax(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st);
 
 hipError_t launch_fused_mfma(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
                              const void* V, float scale, void* O, int out_dtype, hipStream_t st);
