@@ -263,7 +263,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
 #pragma unroll
           for (int j = 0; j < 4; ++j) oacc[b] = mfma32(va[b][j], pf[j], oacc[b]);
       }
-      // the next tile's loads (issued NSLOT-2 tiles ago) have landed
+      // the loads issued NSLOT-2 iterations ago (with two slots: the ones
+      // issued at the top of this iteration, i.e. the next tile) have landed,
+      // and every wavefront is done with this slot
       ring_sync<G::OPS * (NSLOT - 2)>();
     }
   }
