@@ -48,8 +48,8 @@ struct Geo {
   static constexpr int NBW = TB / kDmaBlock / 4;        // loads per wavefront per tile
   static constexpr int RPB = kDmaBlock / RB;            // rows per load
   static constexpr int SLOT = 2 * TB + kBM * 8;         // K tile, V tile, row masks
-  static constexpr int NSLOT = 2;                       // ring depth
-  static constexpr int OPS = 2 * NBW + 1;               // vector-memory ops per wavefront per tile
+  static constexpr int NSLOT = 2;                       // ring depth (the loop waits for
+                                                        // all loads at each barrier)
   static constexpr int LDS = NSLOT * SLOT;
   static constexpr int NKS = D / 16, NDB = D / 32;
 };
@@ -76,8 +76,13 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
     dma16(kbase + row + 16u * (pos ^ swz_k(r)), slot + bk * kDmaBlock);
     dma16(vbase + row + 16u * (pos ^ swz_v(r)), slot + G::TB + bk * kDmaBlock);
   }
-  const uint64_t* mrow = masks + (size_t)max(tl.mask_block, 0) * kBM + wave * 32 + 2 * lane;
-  if (lane < 16) dma16(mrow, slot + 2 * G::TB + wave * 256);
+  // row masks only for tiles with a PARTIAL wavefront (the others never read
+  // them; the ring barrier waits for every outstanding load, so the count of
+  // loads issued per tile may vary)
+  if (tl.mask_block >= 0) {
+    const uint64_t* mrow = masks + (size_t)tl.mask_block * kBM + wave * 32 + 2 * lane;
+    if (lane < 16) dma16(mrow, slot + 2 * G::TB + wave * 256);
+  }
 }
 
 // p = exp2(s * sl2 - m) for this lane's 32 scores, rounded toward zero to bf16
@@ -263,10 +268,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
 #pragma unroll
           for (int j = 0; j < 4; ++j) oacc[b] = mfma32(va[b][j], pf[j], oacc[b]);
       }
-      // the loads issued NSLOT-2 iterations ago (with two slots: the ones
-      // issued at the top of this iteration, i.e. the next tile) have landed,
-      // and every wavefront is done with this slot
-      ring_sync<G::OPS * (NSLOT - 2)>();
+      // the next tile's loads (issued at the top of this iteration) have
+      // landed, and every wavefront is done with this slot
+      ring_sync<0>();
     }
   }
 
