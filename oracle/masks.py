@@ -133,3 +133,39 @@ def dense_mask_row(kind, params, L, i, j=None) -> np.ndarray:
     if kind == "full":
         return np.ones(L, dtype=bool)
     raise ValueError(f"unknown pattern kind {kind!r}")
+
+
+# --------------------------------------------------------------------------
+# Masks given as a union of affine terms (the pattern-descriptor language of
+# the library's C interface, which generalises the per-row affine index map
+# of section 5.1 to row ranges and row groups).  Term t covers rows
+# row_lo <= i < row_hi; with q = floor(i / group) * group its columns are
+# j = j_lo(i) + stride * k for k >= 0 while j <= j_hi(i), where
+# j_lo(i) = lo_i * i + lo_q * q + lo_c and j_hi(i) = hi_i * i + hi_q * q +
+# hi_c, keeping only 0 <= j < L (clamping keeps the residue mod stride).
+def terms_mask_loops(L: int, terms) -> np.ndarray:
+    """The definition above, one term, row and column at a time."""
+    M = np.zeros((L, L), dtype=bool)
+    for t in terms:
+        for i in range(t["row_lo"], t["row_hi"]):
+            q = (i // t["group"]) * t["group"]
+            lo = t["lo_i"] * i + t["lo_q"] * q + t["lo_c"]
+            hi = t["hi_i"] * i + t["hi_q"] * q + t["hi_c"]
+            for j in range(lo, hi + 1, t["stride"]):
+                if 0 <= j < L:
+                    M[i, j] = True
+    return M
+
+
+def terms_mask(L: int, terms) -> np.ndarray:
+    """Same mask, each term evaluated on the whole (i, j) grid at once."""
+    i = np.arange(L, dtype=np.int64)[:, None]
+    j = np.arange(L, dtype=np.int64)[None, :]
+    M = np.zeros((L, L), dtype=bool)
+    for t in terms:
+        q = (i // t["group"]) * t["group"]
+        lo = t["lo_i"] * i + t["lo_q"] * q + t["lo_c"]
+        hi = t["hi_i"] * i + t["hi_q"] * q + t["hi_c"]
+        rows = (i >= t["row_lo"]) & (i < t["row_hi"])
+        M |= rows & (j >= lo) & (j <= hi) & ((j - lo) % t["stride"] == 0)
+    return M

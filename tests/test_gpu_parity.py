@@ -275,3 +275,60 @@ def test_argument_errors(gpu_lib):
     assert rc == 1 and b"aligned" in lib.splat_last_error()
     info = a.info()
     assert info["on_device"] == 1 and info["device"] == torch.cuda.current_device()
+
+
+# --------------------------------------------------------------------------
+# random affine-term descriptors: rows with several runs, strided (gathered)
+# tiles, partial tiles and empty rows, through the fused and unfused paths
+def _random_terms(rng, L):
+    """A band over all rows (stride 1 or 2) plus some of: strided causal
+    columns, a blocked term, global rows -- rows then mix several runs."""
+    def term(r0, r1, lo, hi, stride=1, group=1):
+        return dict(row_lo=r0, row_hi=r1, group=group, lo_i=lo[0], lo_q=lo[1], lo_c=lo[2],
+                    hi_i=hi[0], hi_q=hi[1], hi_c=hi[2], stride=stride)
+    w1, w2 = int(rng.integers(0, L // 3)), int(rng.integers(0, L // 3))
+    terms = [term(0, L, (1, 0, -w1), (1, 0, w2), stride=int(rng.choice([1, 2])))]
+    if rng.random() < 0.6:
+        r0 = int(rng.integers(0, L // 2))
+        s = int(rng.choice([3, 5, 16]))
+        terms.append(term(r0, L, (0, 0, int(rng.integers(0, s))), (1, 0, 0), stride=s))
+    if rng.random() < 0.4:
+        g = int(rng.choice([8, 32, 64]))
+        terms.append(term(0, L, (0, 1, -g), (0, 1, g - 1), group=g))
+    if rng.random() < 0.4:
+        terms.append(term(0, int(rng.integers(1, 40)), (0, 0, 0), (0, 0, L - 1)))
+    return terms
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_descriptor_patterns(gpu_lib, seed):
+    splat = gpu_lib
+    rng = np.random.default_rng(1000 + seed)
+    L = int(rng.integers(40, 400))
+    d = 128 if seed % 3 == 0 else 64
+    dtype = "bf16" if seed % 2 == 0 else "f32"
+    terms = _random_terms(rng, L)
+    print(f"[gpu] random descriptor seed={seed} L={L} d={d} {dtype} terms={terms}", flush=True)
+    M = om.terms_mask(L, terms)
+    try:
+        a = splat.Acsr(splat.Pattern.from_terms(L, terms))
+    except splat.SplatError as e:
+        assert e.name == "UNSUPPORTED"   # a row would need more runs than the format holds
+        pytest.skip(f"seed {seed}: {e}")
+    w = workloads.Workload("random_terms", 1, 2, L, d, dtype, ("terms", ()), 1.0, 2000 + seed)
+    Q, K, V = workloads.make_qkv(w)
+    ref, Sref, Pref = oa.masked_attention(Q, K, V, M, w.scale, want_csr=True)
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O32 = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+    O16 = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.bfloat16)
+    S, P, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    check_O(O32, ref, dtype, f"seed {seed} fused")
+    check_O(O16, ref, "bf16", f"seed {seed} fused out=bf16")
+    check_O(Ou, ref, dtype, f"seed {seed} unfused")
+    rp = om.csr(M)[0]
+    S, P = S.cpu().numpy(), P.cpu().numpy()
+    for h in range(2):
+        assert _rows_normwise_csr(S[0, h], Sref[0, h], rp) <= S_REL
+        if Pref[0, h].size:
+            assert np.abs(P[0, h] - Pref[0, h]).max() <= P_ABS

@@ -193,20 +193,6 @@ def test_random_named_patterns_bit_exact(pat):
     _check_against_mask(a, om.dense_mask(kind, p, L))
 
 
-def _eval_terms(L, terms):
-    """Direct evaluation of the descriptor definition in include/splat.h."""
-    M = np.zeros((L, L), dtype=bool)
-    for t in terms:
-        for i in range(t["row_lo"], t["row_hi"]):
-            qg = (i // t["group"]) * t["group"]
-            lo = t["lo_i"] * i + t["lo_q"] * qg + t["lo_c"]
-            hi = t["hi_i"] * i + t["hi_q"] * qg + t["hi_c"]
-            for j in range(lo, hi + 1, t["stride"]):
-                if 0 <= j < L:
-                    M[i, j] = True
-    return M
-
-
 @st.composite
 def affine_descs(draw):
     L = draw(st.integers(1, 90))
@@ -227,7 +213,7 @@ def affine_descs(draw):
 @given(affine_descs())
 def test_random_affine_descriptors(desc):
     L, terms = desc
-    M = _eval_terms(L, terms)
+    M = om.terms_mask_loops(L, terms)
     try:
         a = splat.Acsr(splat.Pattern.from_terms(L, terms))
     except splat.SplatError as e:

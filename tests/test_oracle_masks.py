@@ -229,3 +229,54 @@ def test_row_masks_equal_dense_mask(kind, params):
     rows = om.row_columns_fast(kind, params, L, range(L))
     for i in range(L):
         np.testing.assert_array_equal(rows[i], np.nonzero(M[i])[0])
+
+
+# --------------------------------------------------------------------------
+# masks from affine-term descriptors
+def _term(row_lo, row_hi, lo, hi, stride=1, group=1):
+    """lo, hi: (coefficient of i, coefficient of q, constant)."""
+    return dict(row_lo=row_lo, row_hi=row_hi, group=group, lo_i=lo[0], lo_q=lo[1], lo_c=lo[2],
+                hi_i=hi[0], hi_q=hi[1], hi_c=hi[2], stride=stride)
+
+
+def test_terms_mask_matches_named_patterns():
+    """Hand-written term lists for the named patterns give their predicates' masks."""
+    L = 97
+    cases = [
+        (("window", {"w": 5}), [_term(0, L, (1, 0, -5), (1, 0, 5))]),
+        (("dilated", {"w": 4, "dilation": 3}), [_term(0, L, (1, 0, -12), (1, 0, 12), stride=3)]),
+        (("blocked", {"block": 8}), [_term(0, L, (0, 1, -8), (0, 1, 7), group=8)]),
+        (("window_global", {"w": 6, "n_global": 4}),
+         [_term(0, L, (1, 0, -6), (1, 0, 6)), _term(0, 4, (0, 0, 0), (0, 0, L - 1)),
+          _term(0, L, (0, 0, 0), (0, 0, 3))]),
+        (("strided_local", {"local": 10, "stride": 7}),
+         [_term(0, L, (1, 0, -9), (1, 0, 0)), _term(0, L, (0, 0, 6), (1, 0, 0), stride=7)]),
+        (("full", {}), [_term(0, L, (0, 0, 0), (0, 0, L - 1))]),
+    ]
+    for (kind, params), terms in cases:
+        ref = om.dense_mask(kind, params, L)
+        np.testing.assert_array_equal(om.terms_mask(L, terms), ref, err_msg=kind)
+        np.testing.assert_array_equal(om.terms_mask_loops(L, terms), ref, err_msg=kind)
+
+
+def test_terms_mask_grid_equals_loops_on_random_terms():
+    rng = np.random.default_rng(11)
+    for _ in range(60):
+        L = int(rng.integers(1, 60))
+        terms = []
+        for _ in range(int(rng.integers(0, 4))):
+            r0 = int(rng.integers(0, L + 1))
+            r1 = int(rng.integers(r0, L + 1))
+            terms.append(_term(r0, r1, (int(rng.integers(-1, 2)), int(rng.integers(-1, 2)),
+                                        int(rng.integers(-30, 30))),
+                               (int(rng.integers(-1, 2)), int(rng.integers(-1, 2)),
+                                int(rng.integers(-30, 70))),
+                               stride=int(rng.choice([1, 2, 3, 7])), group=int(rng.integers(1, 12))))
+        np.testing.assert_array_equal(om.terms_mask(L, terms), om.terms_mask_loops(L, terms))
+
+
+def test_terms_mask_clamping_keeps_the_residue():
+    """Columns below 0 are dropped, not shifted: a stride-3 term starting at -4
+    keeps only columns congruent to -4 (mod 3), i.e. 2, 5, 8, ..."""
+    M = om.terms_mask(12, [_term(0, 1, (0, 0, -4), (0, 0, 11), stride=3)])
+    assert np.flatnonzero(M[0]).tolist() == [2, 5, 8, 11]
