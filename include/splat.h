@@ -225,8 +225,9 @@ splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H
  * with an online (running max / running sum) softmax over the planned key
  * tiles, so S and P never reach device memory.  Q, K, V: [B,H,L,d] of `dtype`;
  * O: [B,H,L,d] of `out_dtype`.  bf16 inputs: scores and softmax in fp32, P
- * rounded to bf16 for the P V product, fp32 accumulation.  fp32 inputs: fp32
- * throughout.  A row without non-zeros gets O = 0.
+ * rounded toward zero to bf16 for the P V product (the row sum adds the same
+ * rounded values), fp32 accumulation.  fp32 inputs: fp32 throughout.  A row
+ * without non-zeros gets O = 0.
  */
 splat_status splat_sparse_mhsa_fwd(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
                                    const void* Q, const void* K, const void* V, float scale,
