@@ -332,3 +332,79 @@ def test_random_descriptor_patterns(gpu_lib, seed):
         assert _rows_normwise_csr(S[0, h], Sref[0, h], rp) <= S_REL
         if Pref[0, h].size:
             assert np.abs(P[0, h] - Pref[0, h]).max() <= P_ABS
+
+
+# --------------------------------------------------------------------------
+# handles built by the paper's analysis pass on explicit masks (two-point
+# affine solve per row, regularity check), through both paths
+@pytest.mark.parametrize("kind,params,L,d,dtype", [
+    ("window", {"w": 37}, 300, 64, "bf16"),
+    ("dilated", {"w": 20, "dilation": 3}, 257, 128, "bf16"),
+    ("blocked", {"block": 32}, 200, 64, "f32"),
+    ("full", {}, 130, 64, "bf16"),
+])
+def test_from_mask_handles(gpu_lib, kind, params, L, d, dtype):
+    splat = gpu_lib
+    print(f"[gpu] from_mask {kind} {params} L={L} d={d} {dtype}", flush=True)
+    M = om.dense_mask(kind, params, L)
+    a = splat.Acsr(mask=M)
+    w = workloads.Workload("from_mask", 2, 2, L, d, dtype, workloads.make_pattern(kind, **params),
+                           1.0, 31 + L)
+    Q, K, V = workloads.make_qkv(w)
+    ref, Sref, Pref = oa.masked_attention(Q, K, V, M, w.scale, want_csr=True)
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+    S, P, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    check_O(O, ref, dtype, "fused")
+    check_O(Ou, ref, dtype, "unfused")
+    rp = om.csr(M)[0]
+    S, P = S.cpu().numpy(), P.cpu().numpy()
+    for b in range(2):
+        for h in range(2):
+            assert _rows_normwise_csr(S[b, h], Sref[b, h], rp) <= S_REL
+            assert np.abs(P[b, h] - Pref[b, h]).max() <= P_ABS
+
+
+def test_many_heads(gpu_lib):
+    """B*H = 600 (not a power of two): the workgroup -> (row group, head) split."""
+    splat = gpu_lib
+    w = workloads.Workload("many_heads", 15, 40, 192, 64, "bf16",
+                           workloads.make_pattern("window_global", w=20, n_global=3), 1.0, 77)
+    print(f"[gpu] many heads B={w.B} H={w.H} L={w.L}", flush=True)
+    Q, K, V = workloads.make_qkv(w)
+    M = om.dense_mask(w.kind, w.params, w.L)
+    ref = oa.masked_attention(Q, K, V, M, w.scale)
+    a = splat.Acsr(splat.Pattern.named(w.kind, w.params, w.L))
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+    _, _, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    check_O(O, ref, "bf16", "fused")
+    check_O(Ou, ref, "bf16", "unfused")
+
+
+def test_maximum_length(gpu_lib):
+    """L = SPLAT_MAX_L = 65536 with a thin window: index arithmetic at the
+    largest size, checked on sampled rows (a dense oracle mask would be 4 GiB)."""
+    splat = gpu_lib
+    L = 65536
+    w = workloads.Workload("max_len", 1, 2, L, 64, "bf16", workloads.make_pattern("window", w=24),
+                           1.0, 99)
+    print(f"[gpu] maximum length L={L}", flush=True)
+    Q, K, V = workloads.make_qkv(w)
+    a = splat.Acsr(splat.Pattern.named(w.kind, w.params, w.L))
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+    _, _, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    O, Ou = O.cpu().numpy(), Ou.cpu().numpy()
+    rng = np.random.default_rng(5)
+    rows = _sample_rows(L, [0, 1, 23, 24, 25, 32767, 32768, L - 26, L - 25, L - 1], rng, 30)
+    cols = om.row_columns_fast(w.kind, w.params, L, rows)
+    q, k, v = oa.to_f64(Q), oa.to_f64(K), oa.to_f64(V)
+    for h in range(2):
+        _, _, Or = oa.attention_rows(q[0, h], k[0, h], v[0, h], rows, cols, w.scale)
+        for name, X in (("fused", O), ("unfused", Ou)):
+            err = float(np.abs(X[0, h, rows] - Or).max())
+            assert err <= BF16_ABS, f"{name} head {h}: {err:.3e}"
