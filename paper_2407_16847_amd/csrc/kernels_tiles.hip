@@ -62,9 +62,11 @@ __device__ __forceinline__ void for_each_key(uint64_t bits, int h, F&& f) {
 // of query row qi.  On FULL tiles the 32 x 64 scores go through a per-
 // wavefront LDS buffer and come back as row segments, so each store writes
 // 4 rows x 256 contiguous bytes (16 lanes per row) instead of 32 rows x 32
-// bytes; on PARTIAL tiles each present score is stored at its rank.
+// bytes; on PARTIAL tiles each present score is stored at its rank.  This is
+// a store stream: occupancy (four wavefronts per SIMD for d = 64) is what
+// keeps enough of it in flight.
 template <int D>
-__global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
+__global__ __launch_bounds__(kTileThreads, D == 64 ? 4 : 2) void k_rsddmm_tiles(
     const Group* __restrict__ groups, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ row_ptr, const Tile* __restrict__ tiles,
     const uint64_t* __restrict__ masks, int L, int BH, int64_t nnz,
@@ -145,8 +147,10 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
         const float4 v = *(const float4*)(stw + r * kStageStride + 4 * cc);
         const int off = __shfl(my_off, r, 64);
         if (off >= 0) {
+          // streamed out: S is far larger than the caches, and dirty S lines
+          // left there slow the kernel that reads S next
           const f32x4u_t o = {v.x, v.y, v.z, v.w};
-          *(f32x4u_t*)(Sh + off + 4 * cc) = o;
+          __builtin_nontemporal_store(o, (f32x4u_t*)(Sh + off + 4 * cc));
         }
       }
     } else if (row_valid) {
@@ -160,24 +164,13 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rsddmm_tiles(
     }
     cnt += popc64(bits);
   };
-  // The next tile's K operands are loaded before this tile's scores are
-  // stored, so waiting for them never waits for the stores (which share the
-  // vector-memory counter); two operand buffers alternate, so no copies.
-  const int tb = grp.tile_begin, te = grp.tile_end;
-  if (tb >= te) return;
-  bf16x8_t kA[2][NKS], kB[2][NKS];
-  Tile tA = tiles[tb];
-  load_k(tA, kA);
-  int t = tb;
-  for (; t + 1 < te; t += 2) {
-    const Tile tB = tiles[t + 1];
-    load_k(tB, kB);
-    tile(tA, kA);
-    tA = tiles[min(t + 2, te - 1)];
-    load_k(tA, kA);
-    tile(tB, kB);
+  for (int t = grp.tile_begin; t < grp.tile_end; ++t) {
+    const Tile tl = tiles[t];
+    if (((tl.flags >> (kWaveShift + 2 * wave)) & 3) == kWaveEmpty) continue;
+    bf16x8_t ka[2][NKS];
+    load_k(tl, ka);
+    tile(tl, ka);
   }
-  if (t < te) tile(tA, kA);
 }
 
 // --------------------------------------------------------------------------
@@ -205,14 +198,16 @@ __device__ __forceinline__ void load4_row(const float* s, int idx, int n, float 
   }
 }
 
+// P is streamed out in 16-byte non-temporal stores: it is far larger than
+// the caches, and dirty P lines left there slow the R-SpMM that reads P next
 __device__ __forceinline__ void store4_row(float* p, int idx, int n, const float (&y)[4]) {
   if (idx + 3 < n) {
     const f32x4u_t v = {y[0], y[1], y[2], y[3]};
-    *(f32x4u_t*)(p + idx) = v;
+    __builtin_nontemporal_store(v, (f32x4u_t*)(p + idx));
   } else {
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      if (idx + e < n) p[idx + e] = y[e];
+      if (idx + e < n) p[idx + e] = y[e];   // single values: ordinary stores
   }
 }
 
