@@ -135,6 +135,24 @@ splat_status splat_pattern_full(int32_t L, splat_pattern_desc* out);
 splat_status splat_acsr_build(const splat_pattern_desc* desc, splat_acsr_t* out);
 
 /*
+ * splat_acsr_build_ex -- splat_acsr_build with planning options, for the
+ * ablation study of section 10 (the R-SpMM kernel with and without span
+ * specialisation, section 8.2).  `flags` is 0 (the same handle as
+ * splat_acsr_build) or SPLAT_PLAN_NO_SPAN: every row group then walks the
+ * whole key range [0, L) in contiguous 64-key tiles and every wavefront that
+ * holds rows evaluates the membership predicate on every tile, including
+ * tiles where none of its rows has a key.  The index set, every compute
+ * call's result and its tolerance are unchanged; only the work differs
+ * (splat_acsr_info's `computed` becomes rows x L, rounded up to tiles).
+ * Returns INVALID_ARG for unknown flag bits and UNSUPPORTED for
+ * SPLAT_PLAN_NO_SPAN with L > SPLAT_NO_SPAN_MAX_L (its per-row masks take
+ * L*L/8 bytes of device memory); otherwise as splat_acsr_build.
+ */
+#define SPLAT_PLAN_NO_SPAN 1u
+#define SPLAT_NO_SPAN_MAX_L 16384
+splat_status splat_acsr_build_ex(const splat_pattern_desc* desc, uint32_t flags, splat_acsr_t* out);
+
+/*
  * splat_acsr_from_mask -- build from an explicit row-major 0/1 byte mask
  * (L*L bytes, host memory) with the paper's analysis pass: per row, the affine
  * indices come from the first two columns (section 5.1, the 2x2 solve) and

@@ -24,11 +24,13 @@ import torch  # loaded first: libsplat then binds to the HIP runtime torch uses
 
 __all__ = [
     "SplatError", "Pattern", "Acsr", "load", "lib_path", "rsddmm", "row_softmax", "rspmm",
-    "sparse_mhsa_fwd", "MAX_RUNS", "MAX_TERMS",
+    "sparse_mhsa_fwd", "MAX_RUNS", "MAX_TERMS", "PLAN_NO_SPAN", "NO_SPAN_MAX_L",
 ]
 
 MAX_TERMS = 8
 MAX_RUNS = 4
+PLAN_NO_SPAN = 1          # SPLAT_PLAN_NO_SPAN
+NO_SPAN_MAX_L = 16384     # SPLAT_NO_SPAN_MAX_L
 F32, BF16 = 0, 1
 _STATUS = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "NOT_REGULAR", 4: "OOM", 5: "HIP",
            6: "NO_DEVICE"}
@@ -84,6 +86,7 @@ def load() -> ctypes.CDLL:
         "splat_pattern_window_global": [i32, i32, i32, P(PatternDesc)],
         "splat_pattern_full": [i32, P(PatternDesc)],
         "splat_acsr_build": [P(PatternDesc), P(vp)],
+        "splat_acsr_build_ex": [P(PatternDesc), ctypes.c_uint32, P(vp)],
         "splat_acsr_from_mask": [i32, vp, P(vp)],
         "splat_acsr_info": [vp, P(AcsrInfo)],
         "splat_acsr_export": [vp, vp, vp],
@@ -194,10 +197,15 @@ class Pattern:
 class Acsr:
     """An ACSR handle: per-row affine runs + work plan, on the current device."""
 
-    def __init__(self, pattern: Optional[Pattern] = None, *, mask: Optional[np.ndarray] = None):
+    def __init__(self, pattern: Optional[Pattern] = None, *, mask: Optional[np.ndarray] = None,
+                 span: bool = True):
+        """span=False plans without span specialisation (every group walks all
+        of [0, L); an ablation, pattern input only)."""
         lib = load()
         h = ctypes.c_void_p()
         if mask is not None:
+            if not span:
+                raise ValueError("span=False needs a pattern, not a mask")
             m = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
             if m.ndim != 2 or m.shape[0] != m.shape[1]:
                 raise ValueError("mask must be a square [L, L] array")
@@ -206,7 +214,11 @@ class Acsr:
         else:
             if pattern is None:
                 raise ValueError("need a pattern or a mask")
-            _check(lib.splat_acsr_build(ctypes.byref(pattern.desc), ctypes.byref(h)))
+            if span:
+                _check(lib.splat_acsr_build(ctypes.byref(pattern.desc), ctypes.byref(h)))
+            else:
+                _check(lib.splat_acsr_build_ex(ctypes.byref(pattern.desc), PLAN_NO_SPAN,
+                                               ctypes.byref(h)))
         self._h = h
         self._lib = lib
         self._info = self.info()

@@ -135,7 +135,8 @@ bool term_ok(const splat_affine_term& t, int32_t L) {
 }  // namespace
 
 // ---------------------------------------------------------------------------
-splat_status build_from_desc(const splat_pattern_desc& d, HostAcsr& a, std::string& err) {
+splat_status build_from_desc(const splat_pattern_desc& d, HostAcsr& a, std::string& err,
+                            uint32_t plan_flags) {
   if (d.L < 1 || d.L > SPLAT_MAX_L) {
     err = "L must be in [1, " + std::to_string(SPLAT_MAX_L) + "], got " + std::to_string(d.L);
     return SPLAT_ERR_INVALID_ARG;
@@ -153,6 +154,7 @@ splat_status build_from_desc(const splat_pattern_desc& d, HostAcsr& a, std::stri
   const int32_t L = d.L;
   a = HostAcsr();
   a.L = L;
+  a.plan_flags = plan_flags;
   a.runs.resize(L);
   a.nruns.assign(L, 0);
   Bits row(L);
@@ -279,29 +281,37 @@ void plan_work(HostAcsr& a) {
           if (x != s) return false;
         return true;
       };
+      // Without span specialisation every group walks the whole key range
+      // [0, L) in contiguous tiles and evaluates the predicate on each.
+      const bool no_span = (a.plan_flags & SPLAT_PLAN_NO_SPAN) != 0;
       int32_t pos = 0;
-      for (int32_t c = U.next(pos); c >= 0; c = U.next(pos)) {
-        const int32_t dense_end = std::min(L - 1, c + kBN - 1);
-        const int32_t k1 = U.count_range(c, dense_end);
-        int32_t k2 = 0, last = c, step = 1;
-        const int32_t nx = U.next(c + 1);
-        if (nx > 0 && nx - c > 1 && gather_ok(nx - c)) {
-          step = nx - c;
-          k2 = 1;
-          while (k2 < kBN) {
-            const int32_t y = U.next(last + 1);
-            if (y < 0 || y - last != step) break;
-            last = y;
-            ++k2;
-          }
-        }
+      for (int32_t c = no_span ? 0 : U.next(pos); c >= 0 && c < L; c = no_span ? pos : U.next(pos)) {
         Tile t{};
-        if (k2 > k1) {
-          t.kb = c, t.ks = step, t.nk = k2;
-          pos = last + 1;
+        if (no_span) {
+          t.kb = c, t.ks = 1, t.nk = std::min(kBN, L - c);
+          pos = c + t.nk;
         } else {
-          t.kb = c, t.ks = 1, t.nk = dense_end - c + 1;
-          pos = dense_end + 1;
+          const int32_t dense_end = std::min(L - 1, c + kBN - 1);
+          const int32_t k1 = U.count_range(c, dense_end);
+          int32_t k2 = 0, last = c, step = 1;
+          const int32_t nx = U.next(c + 1);
+          if (nx > 0 && nx - c > 1 && gather_ok(nx - c)) {
+            step = nx - c;
+            k2 = 1;
+            while (k2 < kBN) {
+              const int32_t y = U.next(last + 1);
+              if (y < 0 || y - last != step) break;
+              last = y;
+              ++k2;
+            }
+          }
+          if (k2 > k1) {
+            t.kb = c, t.ks = step, t.nk = k2;
+            pos = last + 1;
+          } else {
+            t.kb = c, t.ks = 1, t.nk = dense_end - c + 1;
+            pos = dense_end + 1;
+          }
         }
         t.mask_block = -1;
         // per-row membership, per-wavefront state
@@ -318,6 +328,8 @@ void plan_work(HostAcsr& a) {
             empty = empty && rb[m] == 0;
           }
           if (w * kWaveRows >= nrows) full = false;   // no real row: nothing to do
+          // without span specialisation a wavefront with real rows computes every tile
+          if (no_span && w * kWaveRows < nrows) empty = false;
           const int32_t st = empty ? kWaveEmpty : (full ? kWaveFull : kWavePartial);
           t.flags |= st << (kWaveShift + 2 * w);
           group_full = group_full && (st == kWaveFull || w * kWaveRows >= nrows);

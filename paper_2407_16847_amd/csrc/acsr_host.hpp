@@ -26,10 +26,12 @@ struct HostAcsr {
   std::vector<uint64_t> masks;    // kBM row masks per tile with a PARTIAL wavefront
   int64_t computed = 0;           // kWaveRows * kBN per non-empty wavefront tile
   int32_t n_full = 0;
+  uint32_t plan_flags = 0;        // SPLAT_PLAN_* bits the plan was built with
 };
 
 // Union of the descriptor's terms per row -> canonical runs, row_ptr, plan.
-splat_status build_from_desc(const splat_pattern_desc& desc, HostAcsr& out, std::string& err);
+splat_status build_from_desc(const splat_pattern_desc& desc, HostAcsr& out, std::string& err,
+                            uint32_t plan_flags = 0);
 
 // Paper's analysis pass on an explicit 0/1 mask: one affine run per row or
 // SPLAT_ERR_NOT_REGULAR.

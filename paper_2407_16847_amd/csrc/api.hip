@@ -194,19 +194,27 @@ splat_status splat_pattern_full(int32_t L, splat_pattern_desc* out) {
   return splat::pattern_full(L, out) == SPLAT_OK ? ok() : fail(SPLAT_ERR_INVALID_ARG, "bad full pattern arguments");
 }
 
-splat_status splat_acsr_build(const splat_pattern_desc* desc, splat_acsr_t* out) {
+splat_status splat_acsr_build_ex(const splat_pattern_desc* desc, uint32_t flags, splat_acsr_t* out) {
   if (!desc || !out) return fail(SPLAT_ERR_INVALID_ARG, "desc and out must be non-NULL");
+  if (flags & ~SPLAT_PLAN_NO_SPAN) return fail(SPLAT_ERR_INVALID_ARG, "unknown plan flags 0x%x", flags);
+  if ((flags & SPLAT_PLAN_NO_SPAN) && desc->L > SPLAT_NO_SPAN_MAX_L)
+    return fail(SPLAT_ERR_UNSUPPORTED, "SPLAT_PLAN_NO_SPAN needs L <= %d, got %d", SPLAT_NO_SPAN_MAX_L,
+                desc->L);
   splat_acsr* h = new (std::nothrow) splat_acsr();
   if (!h) return fail(SPLAT_ERR_OOM, "host allocation failed");
   std::string err;
   splat_status s;
   try {
-    s = splat::build_from_desc(*desc, h->host, err);
+    s = splat::build_from_desc(*desc, h->host, err, flags);
   } catch (const std::bad_alloc&) {
     s = SPLAT_ERR_OOM;
     err = "host allocation failed during the analysis";
   }
   return finish_build(h, s, err, out);
+}
+
+splat_status splat_acsr_build(const splat_pattern_desc* desc, splat_acsr_t* out) {
+  return splat_acsr_build_ex(desc, 0u, out);
 }
 
 splat_status splat_acsr_from_mask(int32_t L, const uint8_t* mask, splat_acsr_t* out) {

@@ -69,11 +69,13 @@ def _check_against_mask(a, M):
     _check_plan(a, M)
 
 
-def _check_plan(a, M):
+def _check_plan(a, M, span=True):
     """Every non-zero is covered by exactly one (group, tile); tile keys are in
     range and ascending; each tile holds every column of its rows inside its
     key interval; the per-wavefront states (EMPTY / PARTIAL / FULL) and the
-    exported per-row tile masks equal the brute-force mask."""
+    exported per-row tile masks equal the brute-force mask.  Without span
+    specialisation (span=False) every group's tiles are the contiguous 64-key
+    tiles of [0, L), and a wavefront with rows is never EMPTY."""
     L = M.shape[0]
     info = a.info()
     groups, rows, tiles = a.export_plan()
@@ -87,6 +89,11 @@ def _check_plan(a, M):
         prev_end = t1
         grows = rows[off:off + nrows]
         last_hi = -1
+        if not span:
+            starts = [tiles[t][0] for t in range(t0, t1)]
+            assert starts == list(range(0, L, 64)), (g, starts[:4])
+            assert all(tiles[t][1] == 1 and tiles[t][2] == min(64, L - tiles[t][0])
+                       for t in range(t0, t1))
         for t in range(t0, t1):
             kb, ks, nk, flags, mblock = tiles[t]
             assert 1 <= nk <= info["bn"] and ks >= 1
@@ -99,7 +106,7 @@ def _check_plan(a, M):
             for w in range(4):
                 st = (flags >> (8 + 2 * w)) & 3
                 ws = sub[32 * w:32 * (w + 1)]
-                if ws.shape[0] == 0 or not ws.any():
+                if ws.shape[0] == 0 or (span and not ws.any()):
                     want = 0
                 elif nk == info["bn"] and ws.all():
                     want = 3
@@ -310,3 +317,47 @@ def test_empty_and_tiny_masks():
     for L in (1, 2, 3):
         a = splat.Acsr(splat.Pattern.full(L))
         _check_against_mask(a, np.ones((L, L), dtype=bool))
+
+
+# --------------------------------------------------------------------------
+# planning without span specialisation (the ablation of section 8.2)
+@pytest.mark.parametrize("kind,params,L", [
+    ("window", {"w": 4}, 300),
+    ("blocked", {"block": 32}, 256),
+    ("strided_local", {"local": 16, "stride": 16}, 200),
+    ("dilated", {"w": 8, "dilation": 3}, 190),
+    ("window_global", {"w": 20, "n_global": 5}, 260),
+    ("full", {}, 70),
+])
+def test_no_span_plan(kind, params, L):
+    pat = splat.Pattern.named(kind, params, L)
+    a = splat.Acsr(pat, span=False)
+    b = splat.Acsr(pat)
+    M = om.dense_mask(kind, params, L)
+    for x, y in zip(a.export(), b.export()):      # same index set
+        np.testing.assert_array_equal(x, y)
+    _check_plan(a, M, span=False)
+    groups, _, _ = a.export_plan()
+    n_tiles = -(-L // 64)
+    want = sum(32 * 64 * n_tiles * -(-int(g[1]) // 32) for g in groups)
+    assert a.info()["computed"] == want >= b.info()["computed"]
+
+
+def test_no_span_plan_arguments(lib):
+    d = splat.Pattern.window(100, 3).desc
+    h = ctypes.c_void_p()
+    assert lib.splat_acsr_build_ex(ctypes.byref(d), 2, ctypes.byref(h)) == 1
+    assert b"unknown plan flags" in lib.splat_last_error()
+    big = splat.Pattern.window(splat.NO_SPAN_MAX_L + 1, 3).desc
+    assert lib.splat_acsr_build_ex(ctypes.byref(big), splat.PLAN_NO_SPAN, ctypes.byref(h)) == 2
+    assert not h.value
+    with pytest.raises(ValueError):
+        splat.Acsr(mask=np.eye(8, dtype=np.uint8), span=False)
+    a = splat.Acsr(splat.Pattern.window(100, 3), span=True)    # flags 0 == splat_acsr_build
+    assert lib.splat_acsr_build_ex(ctypes.byref(d), 0, ctypes.byref(h)) == 0
+    c = splat.Acsr.__new__(splat.Acsr)
+    c._h, c._lib = h, lib
+    c._info = c.info()
+    assert c.info() == a.info()
+    for x, y in zip(a.export_plan(), c.export_plan()):
+        np.testing.assert_array_equal(x, y)
