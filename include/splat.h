@@ -47,7 +47,9 @@ extern "C" {
 typedef enum {
   SPLAT_OK = 0,
   SPLAT_ERR_INVALID_ARG = 1,  /* null / misaligned pointer, bad size, bad descriptor */
-  SPLAT_ERR_UNSUPPORTED = 2,  /* valid request outside what is implemented (d, runs per row) */
+  SPLAT_ERR_UNSUPPORTED = 2,  /* valid request outside what is implemented: d, runs per row, or a
+                                 bf16 call whose plan needs more than 2^24 (row group, batch*head)
+                                 workgroups (n_groups * B * H, see splat_acsr_info) */
   SPLAT_ERR_NOT_REGULAR = 3,  /* mask input whose rows are not affine-compressible */
   SPLAT_ERR_OOM = 4,          /* host or device allocation failed (build only) */
   SPLAT_ERR_HIP = 5,          /* a HIP runtime call failed; message holds hipGetErrorString */

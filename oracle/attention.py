@@ -112,6 +112,23 @@ def attention_rows(q: np.ndarray, k: np.ndarray, v: np.ndarray,
     return S_out, P_out, O_out
 
 
+def softmax_csr(values, row_ptr) -> np.ndarray:
+    """Softmax of each row of a CSR-ordered value array over the row's entries
+    (section 6: the softmax applied to every row of the compressed matrix).
+
+    values: [nnz] (any float type), row_ptr: [n_rows + 1].  Returns fp64 [nnz];
+    an empty row has no entries and contributes nothing.
+    """
+    x = to_f64(values)
+    out = np.empty_like(x)
+    for i in range(len(row_ptr) - 1):
+        lo, hi = int(row_ptr[i]), int(row_ptr[i + 1])
+        if hi > lo:
+            e = np.exp(x[lo:hi] - x[lo:hi].max())
+            out[lo:hi] = e / e.sum()
+    return out
+
+
 def brute_force(q, k, v, pred, scale: float):
     """Pure-Python loops with math.exp and math.fsum (tiny inputs only).
 

@@ -139,6 +139,17 @@ splat_status check_handle(splat_acsr_t h, int32_t B, int32_t H) {
   return SPLAT_OK;
 }
 
+// The bf16 kernels run one 256-thread workgroup per (row group, batch*head)
+// in a one-dimensional grid, whose work-item count must stay below 2^32.
+splat_status check_tile_grid(splat_acsr_t h, int32_t B, int32_t H) {
+  const int64_t wgs = (int64_t)h->dev.n_groups * B * H;
+  if (wgs * 256 > (int64_t)UINT32_MAX)
+    return fail(SPLAT_ERR_UNSUPPORTED,
+                "the plan's %d row groups x B*H = %lld workgroups exceed one launch (2^24)",
+                h->dev.n_groups, (long long)wgs);
+  return SPLAT_OK;
+}
+
 splat_status check_d(int32_t d) {
   if (d != 64 && d != 128) return fail(SPLAT_ERR_UNSUPPORTED, "d must be 64 or 128, got %d", d);
   return SPLAT_OK;
@@ -325,6 +336,7 @@ splat_status splat_rsddmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t 
   if (h->host.nnz == 0) return ok();
   CHECK(check_ptr(S, "S"));
   hipStream_t st = (hipStream_t)stream;
+  if (dtype == SPLAT_BF16) CHECK(check_tile_grid(h, B, H));
   if (dtype == SPLAT_BF16)
     return launched(splat::launch_rsddmm_tiles(h->dev, B * H, d, Q, K, scale, S, st), "rsddmm");
   return launched(splat::launch_rsddmm_rows(h->dev, dtype, B * H, d, Q, K, scale, S, st), "rsddmm");
@@ -354,6 +366,7 @@ splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H
   CHECK(check_ptr(V, "V"));
   CHECK(check_ptr(O, "O"));
   hipStream_t st = (hipStream_t)stream;
+  if (dtype == SPLAT_BF16) CHECK(check_tile_grid(h, B, H));
   if (dtype == SPLAT_BF16)
     return launched(splat::launch_rspmm_tiles(h->dev, B * H, d, P, V, O, out_dtype, st), "rspmm");
   return launched(splat::launch_rspmm_rows(h->dev, dtype, B * H, d, P, V, O, out_dtype, st), "rspmm");
@@ -371,6 +384,7 @@ splat_status splat_sparse_mhsa_fwd(splat_acsr_t h, splat_dtype dtype, int32_t B,
   CHECK(check_ptr(V, "V"));
   CHECK(check_ptr(O, "O"));
   hipStream_t st = (hipStream_t)stream;
+  if (dtype == SPLAT_BF16) CHECK(check_tile_grid(h, B, H));
   if (dtype == SPLAT_BF16)
     return launched(splat::launch_fused_mfma(h->dev, B * H, d, Q, K, V, scale, O, out_dtype, st),
                     "sparse_mhsa_fwd");

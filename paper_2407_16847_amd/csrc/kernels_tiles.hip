@@ -222,15 +222,55 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Grid: x over blocks of rows, y over batch*head, so that the work-item
+// count of each dimension stays far below 2^32 at every allowed size.
+//
+// Short rows: LPR lanes per row (LPR a power of two below 64, 4*LPR values
+// at most), 64 / LPR rows per wavefront, reductions within the lane segment.
+template <int LPR>
+__global__ __launch_bounds__(256) void k_softmax_seg(const int32_t* __restrict__ row_ptr, int L,
+                                                     int64_t nnz, const float* S, float* P) {
+  constexpr int RPW = 64 / LPR;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int sub = lane & (LPR - 1);
+  const int i = (blockIdx.x * 4 + wave) * RPW + lane / LPR;
+  const int bh = blockIdx.y;
+  int n = 0;
+  size_t base = 0;
+  if (i < L) {
+    const int32_t b0 = row_ptr[i];
+    n = row_ptr[i + 1] - b0;
+    base = (size_t)bh * nnz + b0;
+  }
+  // every lane takes part in the segment reductions; lanes without a row see n = 0
+  float x[4];
+  load4_row(S + base, 4 * sub, n, x);
+  float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+#pragma unroll
+  for (int o = LPR / 2; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  float sum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[e] = ex2_from(x[e], mx);
+    sum += x[e];
+  }
+#pragma unroll
+  for (int o = LPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+  if (n == 0) return;
+  const float inv = 1.f / sum;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] *= inv;
+  store4_row(P + base, 4 * sub, n, x);
+}
+
+// One wavefront per row.
 template <int NV>
 __global__ __launch_bounds__(256) void k_softmax(const int32_t* __restrict__ row_ptr, int L,
-                                                 int64_t n_rows, int64_t nnz, const float* S,
-                                                 float* P) {
+                                                 int64_t nnz, const float* S, float* P) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + wave;
-  if (r >= n_rows) return;
-  const int bh = (int)(r / L);
-  const int i = (int)(r - (int64_t)bh * L);
+  const int i = blockIdx.x * 4 + wave;
+  if (i >= L) return;
+  const int bh = blockIdx.y;
   const int32_t b0 = row_ptr[i];
   const int n = row_ptr[i + 1] - b0;
   if (n == 0) return;
@@ -427,10 +467,17 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
 
 template <int NV>
 hipError_t softmax_launch(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {
-  const int64_t n_rows = (int64_t)a.L * BH;
-  const int64_t blocks = (n_rows + 3) / 4;
-  hipLaunchKernelGGL(k_softmax<NV>, dim3((unsigned)blocks), dim3(256), 0, st, a.row_ptr, a.L,
-                     n_rows, a.nnz, S, P);
+  hipLaunchKernelGGL(k_softmax<NV>, dim3((unsigned)((a.L + 3) / 4), (unsigned)BH), dim3(256), 0,
+                     st, a.row_ptr, a.L, a.nnz, S, P);
+  return hipGetLastError();
+}
+
+template <int LPR>
+hipError_t softmax_seg_launch(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {
+  constexpr int rows_per_block = 4 * (64 / LPR);
+  hipLaunchKernelGGL(k_softmax_seg<LPR>, dim3((unsigned)((a.L + rows_per_block - 1) / rows_per_block),
+                                              (unsigned)BH),
+                     dim3(256), 0, st, a.row_ptr, a.L, a.nnz, S, P);
   return hipGetLastError();
 }
 
@@ -460,6 +507,12 @@ hipError_t launch_rsddmm_tiles(const DevAcsr& a, int BH, int d, const void* Q, c
 
 hipError_t launch_softmax(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {
   const int n = a.max_row_nnz;
+  if (n <= 4) return softmax_seg_launch<1>(a, BH, S, P, st);
+  if (n <= 8) return softmax_seg_launch<2>(a, BH, S, P, st);
+  if (n <= 16) return softmax_seg_launch<4>(a, BH, S, P, st);
+  if (n <= 32) return softmax_seg_launch<8>(a, BH, S, P, st);
+  if (n <= 64) return softmax_seg_launch<16>(a, BH, S, P, st);
+  if (n <= 128) return softmax_seg_launch<32>(a, BH, S, P, st);
   if (n <= 256) return softmax_launch<1>(a, BH, S, P, st);
   if (n <= 512) return softmax_launch<2>(a, BH, S, P, st);
   if (n <= 1024) return softmax_launch<4>(a, BH, S, P, st);

@@ -426,6 +426,81 @@ def test_from_mask_handles(gpu_lib, kind, params, L, d, dtype):
             assert np.abs(P[b, h] - Pref[b, h]).max() <= P_ABS
 
 
+# row softmax on its own, every kernel variant: LPR lanes per row for rows of
+# at most 4 LPR values (LPR = 1 .. 32, with rows that fill their lanes
+# exactly), a wavefront per row up to 2048 values, two passes beyond
+SOFTMAX_ROWS = [
+    ("window", {"w": 0}, 77), ("blocked", {"block": 2}, 300), ("window", {"w": 3}, 129),
+    ("blocked", {"block": 4}, 257), ("window", {"w": 7}, 1000), ("blocked", {"block": 16}, 333),
+    ("window", {"w": 31}, 700), ("window", {"w": 63}, 520), ("window", {"w": 100}, 700),
+    ("window", {"w": 300}, 900), ("window", {"w": 700}, 1500), ("window", {"w": 2100}, 4300),
+]
+
+
+@pytest.mark.parametrize("kind,params,L", SOFTMAX_ROWS)
+def test_softmax_row_lengths(gpu_lib, kind, params, L):
+    splat = gpu_lib
+    a = splat.Acsr(splat.Pattern.named(kind, params, L))
+    rp, _ = a.export()
+    print(f"[gpu] softmax {kind} {params} L={L} max row {a.info()['max_row_nnz']}", flush=True)
+    S = workloads.make_scores(2, 3, a.nnz, seed=L + 7)
+    P = torch.full_like(S, float("nan")).cuda()
+    splat.row_softmax(a, S.cuda(), P)
+    torch.cuda.synchronize()
+    P = P.cpu().numpy()
+    for b in range(2):
+        for h in range(3):
+            err = np.abs(P[b, h] - oa.softmax_csr(S[b, h], rp)).max()
+            assert err <= P_ABS, f"head {(b, h)}: {err:.3e}"
+
+
+def test_softmax_rows_times_heads_beyond_32bit_grid(gpu_lib):
+    """B*H*L = 1040 * 65536 rows of 2-3 values: a grid of 64 lanes per row in
+    one dimension would need 4.4e9 work-items."""
+    splat = gpu_lib
+    B, H, L = 8, 130, 65536
+    a = splat.Acsr(splat.Pattern.window(L, 1))
+    rp, _ = a.export()
+    print(f"[gpu] softmax B*H={B * H} L={L} nnz={a.nnz}", flush=True)
+    S = workloads.make_scores(B, H, a.nnz, seed=41)
+    Sd = S.cuda()
+    P = torch.full_like(Sd, float("nan"))
+    splat.row_softmax(a, Sd, P)
+    counts = torch.from_numpy(np.diff(rp)).long().cuda()
+    row_of = torch.repeat_interleave(torch.arange(L, device="cuda"), counts)
+    sums = torch.zeros((B * H, L), dtype=torch.float64, device="cuda")
+    sums.index_add_(1, row_of, P.view(B * H, -1).double())
+    torch.cuda.synchronize()
+    assert torch.isfinite(P).all(), "every value of every row and head is written"
+    assert (sums - 1).abs().max().item() <= 1e-5
+    for b, h in ((0, 0), (3, 77), (B - 1, H - 1)):
+        for i in (0, 1, 4097, L - 2, L - 1):
+            seg = slice(int(rp[i]), int(rp[i + 1]))
+            ref = oa.softmax_csr(S[b, h, seg], [0, seg.stop - seg.start])
+            assert np.abs(P[b, h, seg].cpu().numpy() - ref).max() <= P_ABS
+
+
+def test_bf16_launch_limit_is_an_error(gpu_lib):
+    """A bf16 call whose plan needs more than 2^24 (row group, batch*head)
+    workgroups is refused before anything is launched."""
+    splat = gpu_lib
+    import ctypes
+    lib = splat.load()
+    a = splat.Acsr(splat.Pattern.window(40000, 1))
+    groups = a.info()["n_groups"]
+    B, H = 5, 13107                              # B*H = 65535
+    assert groups * B * H * 256 > 2 ** 32
+    buf = torch.zeros(1024, dtype=torch.float32, device="cuda")
+    p = ctypes.c_void_p(buf.data_ptr())
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    assert lib.splat_rsddmm(a.handle, 1, B, H, 64, p, p, ctypes.c_float(0.125), p, st) == 2
+    assert b"workgroups" in lib.splat_last_error()
+    assert lib.splat_rspmm(a.handle, 1, B, H, 64, p, p, p, 1, st) == 2
+    assert lib.splat_sparse_mhsa_fwd(a.handle, 1, B, H, 64, p, p, p, ctypes.c_float(0.125), p, 1,
+                                     st) == 2
+    torch.cuda.synchronize()
+
+
 def test_many_heads(gpu_lib):
     """B*H = 600 (not a power of two): the workgroup -> (row group, head) split."""
     splat = gpu_lib

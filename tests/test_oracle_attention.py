@@ -204,3 +204,28 @@ def test_empty_row_gives_zero():
     S, P, O = oa.attention_head(q, k, v, M, 0.5)
     assert (O[2] == 0).all() and (P[2] == 0).all()
     assert np.isfinite(O).all()
+
+
+def test_softmax_csr_pins():
+    """softmax_csr against the dense masked path (a -inf mask, not per-row
+    slices), scipy's softmax on each row, and closed forms."""
+    from scipy.special import softmax as sp_softmax
+    w = workloads.get(3).with_(B=1, H=1, L=260)
+    Q, K, V = workloads.make_qkv(w)
+    M = om.dense_mask(w.kind, w.params, w.L)
+    _, Sc, Pc = oa.masked_attention(Q, K, V, M, w.scale, want_csr=True)
+    row_ptr, _ = om.csr(M)
+    P = oa.softmax_csr(Sc[0, 0], row_ptr)
+    np.testing.assert_allclose(P, Pc[0, 0], rtol=0, atol=1e-15)
+    for i in (0, 1, 129, 259):
+        seg = slice(row_ptr[i], row_ptr[i + 1])
+        np.testing.assert_allclose(P[seg], sp_softmax(Sc[0, 0, seg]), rtol=1e-14, atol=0)
+    # one entry per row -> exactly 1; equal entries -> 1/n; shift invariance; empty rows
+    x = RNG.standard_normal(7)
+    assert (oa.softmax_csr(x, np.arange(8)) == 1.0).all()
+    assert np.allclose(oa.softmax_csr(np.full(5, 3.25), [0, 5]), 0.2, rtol=0, atol=1e-16)
+    v = RNG.standard_normal(9)
+    rp = [0, 4, 4, 9]
+    np.testing.assert_allclose(oa.softmax_csr(v + 100.0, rp), oa.softmax_csr(v, rp), atol=1e-15)
+    out = oa.softmax_csr(v, rp)
+    assert abs(out[:4].sum() - 1) < 1e-15 and abs(out[4:].sum() - 1) < 1e-15

@@ -29,7 +29,7 @@ from typing import Dict, Tuple
 
 import torch
 
-__all__ = ["Workload", "CONFIGS", "get", "make_qkv", "pattern_kinds"]
+__all__ = ["Workload", "CONFIGS", "get", "make_qkv", "make_scores", "pattern_kinds"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -112,3 +112,10 @@ def make_qkv(w: Workload, device: str = "cpu"):
             raise ValueError(f"unknown dtype {w.dtype!r}")
         out.append(x.contiguous().to(device))
     return tuple(out)
+
+
+def make_scores(B: int, H: int, nnz: int, seed: int, std: float = 3.0):
+    """Scores [B, H, nnz] fp32 for exercising the row softmax on its own:
+    ``torch.Generator('cpu').manual_seed(seed)``, N(0, 1) times ``std``."""
+    g = torch.Generator("cpu").manual_seed(int(seed))
+    return (torch.randn((B, H, nnz), generator=g, dtype=torch.float32) * std).contiguous()
