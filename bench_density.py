@@ -16,6 +16,10 @@ eager calls, host cost included.  Per point:
 * the unfused chain (splat_rsddmm, splat_row_softmax, splat_rspmm), each step,
 * R-SpMM, R-SDDMM and the fused forward on a plan without span
   specialisation (SPLAT_PLAN_NO_SPAN: every row group walks all of [0, L)),
+* the data-layout comparison: the transpose to the column-compressed,
+  column-major layout and R-SpMM reading it, against R-SpMM on the
+  row-major values the softmax leaves (masks whose columns are single
+  affine runs; the paper's switch takes the column-major layout from 10%),
 * dense references on the same GPU: torch.matmul (hipBLASLt) for the dense
   products Q K^T and P V that a dense-library chain computes in place of
   R-SDDMM and R-SpMM, and torch's scaled_dot_product_attention with the mask
@@ -164,6 +168,16 @@ def main() -> int:
                 "fused_eager": timed(lambda: splat.sparse_mhsa_fwd(a, Q, K, V, scale, O=O),
                                      args.reps),
             }
+            ac = splat.Acsr(pat, columns=True)
+            if ac.info()["columns"] == 1:
+                Pt = torch.empty_like(P)
+                t["transpose"] = graph_timed(lambda: splat.transpose_colmajor(ac, P, Pt), args.reps)
+                t["rspmm_colmajor"] = graph_timed(lambda: splat.rspmm_colmajor(ac, Pt, V, O=O),
+                                                  args.reps)
+                del Pt
+            else:
+                t["transpose"] = t["rspmm_colmajor"] = None
+            ac.close()
             ns = splat.Acsr(pat, span=False)
             t["rspmm_nospan"] = graph_timed(lambda: splat.rspmm(ns, P, V, O=O), args.reps)
             t["rsddmm_nospan"] = graph_timed(lambda: splat.rsddmm(ns, Q, K, scale, S=S), args.reps)
@@ -179,6 +193,8 @@ def main() -> int:
                    "fused_TFLOPs": round(flops / t["fused"] / 1e6, 1),
                    "unfused_us": r(t["rsddmm"] + t["softmax"] + t["rspmm"]),
                    "span_speedup_rspmm": round(t["rspmm_nospan"] / t["rspmm"], 2),
+                   "switch_picks_colmajor": bool(t["transpose"] is not None
+                                                 and nnz / (L * L) >= splat.DENSE_ALPHA),
                    **{f"{k}_us": r(v) for k, v in t.items()},
                    **{f"dense_{k}": r(v) for k, v in dense.items()}}
             rows.append(row)
@@ -192,14 +208,15 @@ def main() -> int:
 
     print("\n| family | params | density | fused µs | fused TFLOP/s | fused eager µs | "
           "R-SDDMM µs | softmax µs | R-SpMM µs | R-SpMM no span µs | span speedup | "
-          "fused no span µs | dense masked SDPA µs |")
-    print("|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+          "fused no span µs | transpose + col-major R-SpMM µs | dense masked SDPA µs |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
     for x in rows:
         ps = ",".join(f"{k}={v}" for k, v in x["params"].items())
         print(f"| {x['family']} | {ps} | {100 * x['density']:.2f}% | {f(x['fused_us'])} | "
               f"{f(x['fused_TFLOPs'])} | {f(x['fused_eager_us'])} | {f(x['rsddmm_us'])} | "
               f"{f(x['softmax_us'])} | {f(x['rspmm_us'])} | {f(x['rspmm_nospan_us'])} | "
               f"{f(x['span_speedup_rspmm'])} | {f(x['fused_nospan_us'])} | "
+              f"{f(x['transpose_us'])} + {f(x['rspmm_colmajor_us'])} | "
               f"{f(x['dense_masked_us'])} |")
     print(f"\ndense, independent of the mask: flash SDPA {f(r(dense['flash_us']))} µs, "
           f"matmul Q K^T {f(r(dense['qk_matmul_us']))} µs, "

@@ -137,20 +137,31 @@ splat_status splat_pattern_full(int32_t L, splat_pattern_desc* out);
 splat_status splat_acsr_build(const splat_pattern_desc* desc, splat_acsr_t* out);
 
 /*
- * splat_acsr_build_ex -- splat_acsr_build with planning options, for the
- * ablation study of section 10 (the R-SpMM kernel with and without span
- * specialisation, section 8.2).  `flags` is 0 (the same handle as
- * splat_acsr_build) or SPLAT_PLAN_NO_SPAN: every row group then walks the
- * whole key range [0, L) in contiguous 64-key tiles and every wavefront that
- * holds rows evaluates the membership predicate on every tile, including
- * tiles where none of its rows has a key.  The index set, every compute
- * call's result and its tolerance are unchanged; only the work differs
- * (splat_acsr_info's `computed` becomes rows x L, rounded up to tiles).
- * Returns INVALID_ARG for unknown flag bits and UNSUPPORTED for
- * SPLAT_PLAN_NO_SPAN with L > SPLAT_NO_SPAN_MAX_L (its per-row masks take
- * L*L/8 bytes of device memory); otherwise as splat_acsr_build.
+ * splat_acsr_build_ex -- splat_acsr_build with planning options.  `flags` is
+ * 0 (the same handle as splat_acsr_build) or a combination of:
+ *
+ * SPLAT_PLAN_NO_SPAN -- for the ablation study of section 10 (the R-SpMM
+ *   kernel with and without span specialisation, section 8.2): every row
+ *   group walks the whole key range [0, L) in contiguous 64-key tiles and
+ *   every wavefront that holds rows evaluates the membership predicate on
+ *   every tile, including tiles where none of its rows has a key.  The index
+ *   set, every compute call's result and its tolerance are unchanged; only
+ *   the work differs (splat_acsr_info's `computed` becomes rows x L, rounded
+ *   up to tiles).  UNSUPPORTED with L > SPLAT_NO_SPAN_MAX_L (its per-row
+ *   masks take L*L/8 bytes of device memory).
+ * SPLAT_PLAN_COLUMNS -- the column-wise analysis of section 5.2 (a regular
+ *   mask is also column-wise affine-compressible): when every column's rows
+ *   form one affine run, the handle also describes the column-compressed,
+ *   column-major value layout (splat_acsr_export_csc,
+ *   splat_transpose_colmajor, splat_rspmm_colmajor); splat_acsr_info's
+ *   `columns` reports the outcome.  A mask whose columns are not single runs
+ *   still builds (columns = 0).  O(nnz) host time; UNSUPPORTED above 2^28
+ *   non-zeros per head.
+ *
+ * Returns INVALID_ARG for unknown flag bits; otherwise as splat_acsr_build.
  */
 #define SPLAT_PLAN_NO_SPAN 1u
+#define SPLAT_PLAN_COLUMNS 2u
 #define SPLAT_NO_SPAN_MAX_L 16384
 splat_status splat_acsr_build_ex(const splat_pattern_desc* desc, uint32_t flags, splat_acsr_t* out);
 
@@ -179,12 +190,24 @@ typedef struct {
   int32_t n_full_tiles;
   int64_t nnz;             /* non-zeros per (batch, head) */
   int64_t computed;        /* rows x keys of the 32-row x 64-key tiles the kernels compute (>= nnz) */
+  int32_t columns;         /* column-wise analysis: -1 not requested, 0 some column is not one
+                              affine run, 1 every column is (column-major layout available) */
+  int32_t reserved;
 } splat_acsr_info_t;
 
 splat_status splat_acsr_info(splat_acsr_t h, splat_acsr_info_t* out);
 
 /* Host copies of the index set: row_ptr[L+1] and col_idx[nnz] (CSR order). */
 splat_status splat_acsr_export(splat_acsr_t h, int32_t* row_ptr, int32_t* col_idx);
+
+/*
+ * Host copies of the transposed index set: col_ptr[L+1] and row_idx[nnz] in
+ * column-compressed order (column by column, ascending row), which is also
+ * the value order of the column-major layout.  Needs a handle built with
+ * SPLAT_PLAN_COLUMNS whose columns are single runs: INVALID_ARG without the
+ * analysis, NOT_REGULAR when some column is not one affine run.
+ */
+splat_status splat_acsr_export_csc(splat_acsr_t h, int32_t* col_ptr, int32_t* row_idx);
 
 /* Runs of one row: runs[3*r + {0,1,2}] = (start, stride, count), r < *nruns. */
 splat_status splat_acsr_row_runs(splat_acsr_t h, int32_t row, int32_t* runs, int32_t* nruns);
@@ -239,6 +262,54 @@ splat_status splat_row_softmax(splat_acsr_t h, int32_t B, int32_t H, const float
  */
 splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
                          const float* P, const void* V, void* O, splat_dtype out_dtype, void* stream);
+
+/*
+ * splat_transpose_colmajor -- the data-layout reordering of section 9: the
+ * values of every (batch, head) moved from the row-compressed, row-major
+ * order (CSR order, as splat_rsddmm and splat_row_softmax write them) to the
+ * column-compressed, column-major order of section 5.2 (column by column,
+ * ascending row; the order of splat_acsr_export_csc):
+ *   Pt[b,h, col_ptr[j] + t] = P[b,h, row_ptr[i] + k]
+ * where row i is the t-th row of column j and j the k-th column of row i.
+ * P, Pt: fp32 [B,H,nnz], distinct, non-overlapping.  The handle must have
+ * been built with SPLAT_PLAN_COLUMNS and have single-run columns
+ * (INVALID_ARG / NOT_REGULAR otherwise).  A pure permutation: bit-exact.
+ */
+splat_status splat_transpose_colmajor(splat_acsr_t h, int32_t B, int32_t H, const float* P, float* Pt,
+                                      void* stream);
+
+/*
+ * splat_rspmm_colmajor -- splat_rspmm reading P in the column-compressed,
+ * column-major layout (section 9: the layout the paper selects for dense
+ * masks so that consecutive rows of a column are read from consecutive
+ * addresses).  Pt as written by splat_transpose_colmajor; every other
+ * argument, the result and its rounding as splat_rspmm (with bf16 V the
+ * result equals splat_rspmm's bit for bit).  Handle requirements as
+ * splat_transpose_colmajor.
+ */
+splat_status splat_rspmm_colmajor(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                                  const float* Pt, const void* V, void* O, splat_dtype out_dtype,
+                                  void* stream);
+
+/*
+ * splat_sparse_mhsa_unfused -- the paper's unfused chain with its density
+ * switch (section 9: analysis pass, data-layout reordering): S = R-SDDMM,
+ * P = softmax of S in place, then, when the mask's density nnz / L^2 is at
+ * least `alpha` and the handle has the column-major layout
+ * (SPLAT_PLAN_COLUMNS with single-run columns), Pt = the column-major copy
+ * of P and O = splat_rspmm_colmajor(Pt); otherwise O = splat_rspmm(P).  The
+ * paper's threshold is alpha = 0.10 (SPLAT_DENSE_ALPHA); alpha > 1 never
+ * transposes.  S: fp32 [B,H,nnz] workspace (holds P afterwards); Pt: fp32
+ * [B,H,nnz] workspace, used (and required non-NULL) only on the column-major
+ * branch.  *used_colmajor (if non-NULL) is set to 1 on the column-major
+ * branch, 0 otherwise.  Results as the individual calls.
+ */
+#define SPLAT_DENSE_ALPHA 0.10f
+splat_status splat_sparse_mhsa_unfused(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H,
+                                       int32_t d, const void* Q, const void* K, const void* V,
+                                       float scale, float* S, float* Pt, void* O,
+                                       splat_dtype out_dtype, float alpha, int32_t* used_colmajor,
+                                       void* stream);
 
 /*
  * splat_sparse_mhsa_fwd -- the three steps fused: O = softmax_nz(scale * M (x) Q K^T) V

@@ -96,6 +96,29 @@ def csr(mask: np.ndarray):
     return row_ptr, col_idx
 
 
+def csc(mask: np.ndarray):
+    """(col_ptr int64[L+1], row_idx int64[nnz]) of a boolean mask: rows in
+    ascending order within each column, column by column -- the order the
+    column-compressed column-major layout stores the values in (section 5.2).
+    Traverses the mask column by column (Fortran order)."""
+    mask = np.asarray(mask, dtype=bool)
+    counts = mask.sum(axis=0).astype(np.int64)
+    col_ptr = np.zeros(mask.shape[1] + 1, dtype=np.int64)
+    np.cumsum(counts, out=col_ptr[1:])
+    cols_major = np.nonzero(mask.T)                      # (column, row) pairs, column-major
+    row_idx = cols_major[1].astype(np.int64)
+    return col_ptr, row_idx
+
+
+def colmajor_source(mask: np.ndarray) -> np.ndarray:
+    """For every slot of the column-major value order, the CSR (row-major)
+    position of the same (row, column) entry: colmajor = csr_values[this]."""
+    mask = np.asarray(mask, dtype=bool)
+    pos = np.full(mask.shape, -1, dtype=np.int64)
+    pos[mask] = np.arange(int(mask.sum()), dtype=np.int64)  # row-major numbering
+    return pos.T[mask.T]                                     # read back column by column
+
+
 def row_columns(kind: str, params: Dict[str, int], L: int, i: int) -> np.ndarray:
     """Ascending key columns of one row, by brute force over every j."""
     f = predicate(kind, params)

@@ -24,12 +24,15 @@ import torch  # loaded first: libsplat then binds to the HIP runtime torch uses
 
 __all__ = [
     "SplatError", "Pattern", "Acsr", "load", "lib_path", "rsddmm", "row_softmax", "rspmm",
-    "sparse_mhsa_fwd", "MAX_RUNS", "MAX_TERMS", "PLAN_NO_SPAN", "NO_SPAN_MAX_L",
+    "sparse_mhsa_fwd", "MAX_RUNS", "MAX_TERMS", "PLAN_NO_SPAN", "NO_SPAN_MAX_L", "PLAN_COLUMNS",
+    "DENSE_ALPHA", "transpose_colmajor", "rspmm_colmajor", "sparse_mhsa_unfused",
 ]
 
 MAX_TERMS = 8
 MAX_RUNS = 4
 PLAN_NO_SPAN = 1          # SPLAT_PLAN_NO_SPAN
+PLAN_COLUMNS = 2          # SPLAT_PLAN_COLUMNS
+DENSE_ALPHA = 0.10        # SPLAT_DENSE_ALPHA
 NO_SPAN_MAX_L = 16384     # SPLAT_NO_SPAN_MAX_L
 F32, BF16 = 0, 1
 _STATUS = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "NOT_REGULAR", 4: "OOM", 5: "HIP",
@@ -56,7 +59,8 @@ class AcsrInfo(ctypes.Structure):
     _fields_ = [("L", ctypes.c_int32), ("max_row_nnz", ctypes.c_int32), ("max_runs", ctypes.c_int32),
                 ("on_device", ctypes.c_int32), ("device", ctypes.c_int32), ("bm", ctypes.c_int32),
                 ("bn", ctypes.c_int32), ("n_groups", ctypes.c_int32), ("n_tiles", ctypes.c_int32),
-                ("n_full_tiles", ctypes.c_int32), ("nnz", ctypes.c_int64), ("computed", ctypes.c_int64)]
+                ("n_full_tiles", ctypes.c_int32), ("nnz", ctypes.c_int64), ("computed", ctypes.c_int64),
+                ("columns", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 _LIB: Optional[ctypes.CDLL] = None
@@ -97,6 +101,11 @@ def load() -> ctypes.CDLL:
         "splat_row_softmax": [vp, i32, i32, vp, vp, vp],
         "splat_rspmm": [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp],
         "splat_sparse_mhsa_fwd": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, i32, vp],
+        "splat_acsr_export_csc": [vp, vp, vp],
+        "splat_transpose_colmajor": [vp, i32, i32, vp, vp, vp],
+        "splat_rspmm_colmajor": [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp],
+        "splat_sparse_mhsa_unfused": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, i32, f32,
+                                      P(i32), vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -198,14 +207,17 @@ class Acsr:
     """An ACSR handle: per-row affine runs + work plan, on the current device."""
 
     def __init__(self, pattern: Optional[Pattern] = None, *, mask: Optional[np.ndarray] = None,
-                 span: bool = True):
+                 span: bool = True, columns: bool = False):
         """span=False plans without span specialisation (every group walks all
-        of [0, L); an ablation, pattern input only)."""
+        of [0, L); an ablation).  columns=True adds the column-wise analysis
+        (the column-major layout when every column is one affine run).  Both
+        need a pattern, not a mask."""
         lib = load()
         h = ctypes.c_void_p()
+        flags = (0 if span else PLAN_NO_SPAN) | (PLAN_COLUMNS if columns else 0)
         if mask is not None:
-            if not span:
-                raise ValueError("span=False needs a pattern, not a mask")
+            if flags:
+                raise ValueError("span=False and columns=True need a pattern, not a mask")
             m = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
             if m.ndim != 2 or m.shape[0] != m.shape[1]:
                 raise ValueError("mask must be a square [L, L] array")
@@ -214,11 +226,10 @@ class Acsr:
         else:
             if pattern is None:
                 raise ValueError("need a pattern or a mask")
-            if span:
+            if flags == 0:
                 _check(lib.splat_acsr_build(ctypes.byref(pattern.desc), ctypes.byref(h)))
             else:
-                _check(lib.splat_acsr_build_ex(ctypes.byref(pattern.desc), PLAN_NO_SPAN,
-                                               ctypes.byref(h)))
+                _check(lib.splat_acsr_build_ex(ctypes.byref(pattern.desc), flags, ctypes.byref(h)))
         self._h = h
         self._lib = lib
         self._info = self.info()
@@ -259,6 +270,14 @@ class Acsr:
         _check(self._lib.splat_acsr_export(self.handle, rp.ctypes.data_as(ctypes.c_void_p),
                                            ci.ctypes.data_as(ctypes.c_void_p)))
         return rp, ci[: self.nnz]
+
+    def export_csc(self) -> Tuple[np.ndarray, np.ndarray]:
+        """(col_ptr [L+1], row_idx [nnz]): the column-major value order."""
+        cp = np.zeros(self.L + 1, dtype=np.int32)
+        ri = np.zeros(max(self.nnz, 1), dtype=np.int32)
+        _check(self._lib.splat_acsr_export_csc(self.handle, cp.ctypes.data_as(ctypes.c_void_p),
+                                               ri.ctypes.data_as(ctypes.c_void_p)))
+        return cp, ri[: self.nnz]
 
     def row_runs(self, row: int):
         buf = np.zeros(3 * MAX_RUNS, dtype=np.int32)
@@ -381,3 +400,73 @@ def sparse_mhsa_fwd(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, V: torch.Tenso
                                         V.data_ptr(), float(scale), O.data_ptr(), _DT[O.dtype],
                                         _stream()))
     return O
+
+
+def _values(x: torch.Tensor, name: str, acsr: Acsr, B: int, H: int) -> None:
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if x.dtype != torch.float32 or tuple(x.shape) != (B, H, acsr.nnz) or not x.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 [B, H, {acsr.nnz}] tensor")
+
+
+def transpose_colmajor(acsr: Acsr, P: torch.Tensor, Pt: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """P (CSR value order) -> Pt (column-compressed, column-major order)."""
+    if P.dim() != 3:
+        raise ValueError("P must be [B, H, nnz]")
+    B, H, _ = P.shape
+    _values(P, "P", acsr, B, H)
+    if Pt is None:
+        Pt = torch.empty_like(P)
+    _values(Pt, "Pt", acsr, B, H)
+    _check(load().splat_transpose_colmajor(acsr.handle, B, H, P.data_ptr() if P.numel() else None,
+                                           Pt.data_ptr() if Pt.numel() else None, _stream()))
+    return Pt
+
+
+def rspmm_colmajor(acsr: Acsr, Pt: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor] = None,
+                   out_dtype: Optional[torch.dtype] = None) -> torch.Tensor:
+    """O = P V with P given in the column-major value order."""
+    _dense(V, "V", acsr)
+    B, H, L, d = V.shape
+    _values(Pt, "Pt", acsr, B, H)
+    odt = _out_dtype(out_dtype if O is None else O.dtype, V.dtype)
+    if O is None:
+        O = torch.empty((B, H, L, d), dtype=odt, device=V.device)
+    else:
+        _dense(O, "O", acsr, d)
+    _check(load().splat_rspmm_colmajor(acsr.handle, _DT[V.dtype], B, H, d,
+                                       Pt.data_ptr() if Pt.numel() else None, V.data_ptr(),
+                                       O.data_ptr(), _DT[O.dtype], _stream()))
+    return O
+
+
+def sparse_mhsa_unfused(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, scale: float,
+                        alpha: float = DENSE_ALPHA, S: Optional[torch.Tensor] = None,
+                        Pt: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
+                        out_dtype: Optional[torch.dtype] = None):
+    """The unfused chain with the density switch; returns (O, used_colmajor).
+    S (and, for a column-major run, Pt) are fp32 [B, H, nnz] workspaces."""
+    _dense(Q, "Q", acsr)
+    B, H, L, d = Q.shape
+    for n, x in (("K", K), ("V", V)):
+        _dense(x, n, acsr, d)
+        if x.dtype != Q.dtype or x.shape[:2] != Q.shape[:2]:
+            raise ValueError(f"{n} must match Q in dtype, B and H")
+    if S is None:
+        S = torch.empty((B, H, acsr.nnz), dtype=torch.float32, device=Q.device)
+    _values(S, "S", acsr, B, H)
+    if Pt is None and acsr.info()["columns"] == 1:
+        Pt = torch.empty_like(S)
+    if Pt is not None:
+        _values(Pt, "Pt", acsr, B, H)
+    odt = _out_dtype(out_dtype if O is None else O.dtype, Q.dtype)
+    if O is None:
+        O = torch.empty((B, H, L, d), dtype=odt, device=Q.device)
+    else:
+        _dense(O, "O", acsr, d)
+    used = ctypes.c_int32(-1)
+    _check(load().splat_sparse_mhsa_unfused(
+        acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(), V.data_ptr(), float(scale),
+        S.data_ptr() if S.numel() else None, Pt.data_ptr() if Pt is not None and Pt.numel() else None,
+        O.data_ptr(), _DT[O.dtype], float(alpha), ctypes.byref(used), _stream()))
+    return O, bool(used.value)

@@ -53,6 +53,14 @@ struct RowRuns {
   Run r[SPLAT_MAX_RUNS];   // unused runs have count == 0
 };
 
+// A column held as one affine run of rows (column-wise affine
+// compressibility, section 5.2): rows start + stride * t for t < count, whose
+// values sit at ptr + t of the head's column-compressed, column-major value
+// array (ptr = the column's offset in that array).
+struct ColRun {
+  int32_t start, stride, count, ptr;
+};
+
 struct Group {
   int32_t row_off, nrows, tile_begin, tile_end;
 };

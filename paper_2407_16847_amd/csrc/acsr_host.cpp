@@ -124,6 +124,50 @@ splat_status finish_rows(HostAcsr& a, std::string& err) {
   return SPLAT_OK;
 }
 
+// Column-wise analysis (section 5.2): the mask's transpose is affine-
+// compressible when every column's rows form one affine run.  Rows are
+// visited in ascending order, so each column's rows arrive sorted; a column
+// is one run iff every gap equals its first gap.
+splat_status analyse_columns(HostAcsr& a, std::string& err) {
+  const int32_t L = a.L;
+  if (a.nnz > (int64_t(1) << 28)) {
+    err = "the column-wise analysis is limited to 2^28 non-zeros per head";
+    return SPLAT_ERR_UNSUPPORTED;
+  }
+  std::vector<ColRun> c(L, ColRun{0, 1, 0, 0});
+  std::vector<int32_t> last(L, -1);
+  bool regular = true;
+  for (int32_t i = 0; i < L && regular; ++i) {
+    for (int r = 0; r < SPLAT_MAX_RUNS && regular; ++r) {
+      const Run& q = a.runs[i].r[r];
+      for (int32_t k = 0; k < q.count; ++k) {
+        const int32_t j = q.start + q.stride * k;
+        ColRun& cj = c[j];
+        if (cj.count == 0) {
+          cj.start = i;
+        } else if (cj.count == 1) {
+          cj.stride = i - cj.start;
+        } else if (i - last[j] != cj.stride) {
+          regular = false;
+          break;
+        }
+        last[j] = i;
+        ++cj.count;
+      }
+    }
+  }
+  a.cols.clear();
+  a.col_regular = regular ? 1 : 0;
+  if (!regular) return SPLAT_OK;
+  int64_t ptr = 0;
+  for (int32_t j = 0; j < L; ++j) {
+    c[j].ptr = (int32_t)ptr;
+    ptr += c[j].count;
+  }
+  a.cols = std::move(c);
+  return SPLAT_OK;
+}
+
 bool term_ok(const splat_affine_term& t, int32_t L) {
   const int32_t lim = 1 << 20;
   auto small = [&](int32_t v) { return v >= -lim && v <= lim; };
@@ -184,7 +228,9 @@ splat_status build_from_desc(const splat_pattern_desc& d, HostAcsr& a, std::stri
     }
     a.nruns[i] = nr;
   }
-  return finish_rows(a, err);
+  splat_status s = finish_rows(a, err);
+  if (s == SPLAT_OK && (plan_flags & SPLAT_PLAN_COLUMNS)) s = analyse_columns(a, err);
+  return s;
 }
 
 splat_status build_from_mask(int32_t L, const uint8_t* mask, HostAcsr& a, std::string& err) {

@@ -27,6 +27,10 @@ struct HostAcsr {
   int64_t computed = 0;           // kWaveRows * kBN per non-empty wavefront tile
   int32_t n_full = 0;
   uint32_t plan_flags = 0;        // SPLAT_PLAN_* bits the plan was built with
+  // column-wise analysis (SPLAT_PLAN_COLUMNS): -1 not done, 0 some column is
+  // not one affine run, 1 every column is; cols[j] describes column j
+  int32_t col_regular = -1;
+  std::vector<ColRun> cols;       // L when col_regular == 1
 };
 
 // Union of the descriptor's terms per row -> canonical runs, row_ptr, plan.

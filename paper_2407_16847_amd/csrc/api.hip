@@ -58,7 +58,8 @@ splat_status upload(splat_acsr* h) {
   const size_t s_tiles = al(sizeof(splat::Tile) * (a.tiles.size() + 1));
   // one extra zero block: tiles without masks still issue (unused) mask loads
   const size_t s_masks = al(sizeof(uint64_t) * (a.masks.size() + splat::kBM));
-  const size_t total = s_rowptr + s_runs + s_rows + s_groups + s_tiles + s_masks;
+  const size_t s_cols = al(sizeof(splat::ColRun) * a.cols.size());
+  const size_t total = s_rowptr + s_runs + s_rows + s_groups + s_tiles + s_masks + s_cols;
   void* mem = nullptr;
   e = hipMalloc(&mem, total);
   if (e != hipSuccess) {
@@ -79,9 +80,10 @@ splat_status upload(splat_acsr* h) {
                {a.rows.data(), sizeof(int32_t) * a.L, s_rows},
                {a.groups.data(), sizeof(splat::Group) * a.groups.size(), s_groups},
                {a.tiles.data(), sizeof(splat::Tile) * a.tiles.size(), s_tiles},
-               {a.masks.data(), sizeof(uint64_t) * a.masks.size(), s_masks}};
-  char* dst[6];
-  for (int k = 0; k < 6; ++k) {
+               {a.masks.data(), sizeof(uint64_t) * a.masks.size(), s_masks},
+               {a.cols.data(), sizeof(splat::ColRun) * a.cols.size(), s_cols}};
+  char* dst[7];
+  for (int k = 0; k < 7; ++k) {
     dst[k] = p;
     if (parts[k].n) {
       e = hipMemcpy(p, parts[k].src, parts[k].n, hipMemcpyHostToDevice);
@@ -104,6 +106,7 @@ splat_status upload(splat_acsr* h) {
   h->dev.groups = (const splat::Group*)dst[3];
   h->dev.tiles = (const splat::Tile*)dst[4];
   h->dev.masks = (const uint64_t*)dst[5];
+  h->dev.cols = a.cols.empty() ? nullptr : (const splat::ColRun*)dst[6];
   return SPLAT_OK;
 }
 
@@ -150,6 +153,15 @@ splat_status check_tile_grid(splat_acsr_t h, int32_t B, int32_t H) {
   return SPLAT_OK;
 }
 
+// The column-major layout needs the column-wise analysis and single-run columns.
+splat_status check_columns(splat_acsr_t h) {
+  if (h->host.col_regular < 0)
+    return fail(SPLAT_ERR_INVALID_ARG, "the handle was built without SPLAT_PLAN_COLUMNS");
+  if (h->host.col_regular == 0)
+    return fail(SPLAT_ERR_NOT_REGULAR, "some column of the mask is not one affine run of rows");
+  return SPLAT_OK;
+}
+
 splat_status check_d(int32_t d) {
   if (d != 64 && d != 128) return fail(SPLAT_ERR_UNSUPPORTED, "d must be 64 or 128, got %d", d);
   return SPLAT_OK;
@@ -177,6 +189,57 @@ splat_status launched(hipError_t e, const char* what) {
     splat_status _s = (x);           \
     if (_s != SPLAT_OK) return _s;   \
   } while (0)
+
+// Validation of an R-SpMM call (row-major or column-major values).
+splat_status check_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                         const float* P, const void* V, const void* O, splat_dtype out_dtype,
+                         bool colmajor) {
+  CHECK(check_handle(h, B, H));
+  CHECK(check_dtype(dtype, "dtype"));
+  CHECK(check_dtype(out_dtype, "out_dtype"));
+  CHECK(check_d(d));
+  if (colmajor) CHECK(check_columns(h));
+  if (h->host.nnz > 0) CHECK(check_ptr(P, "P"));
+  CHECK(check_ptr(V, "V"));
+  CHECK(check_ptr(O, "O"));
+  if (dtype == SPLAT_BF16) CHECK(check_tile_grid(h, B, H));
+  return SPLAT_OK;
+}
+
+splat_status launch_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                          const float* P, const void* V, void* O, splat_dtype out_dtype,
+                          bool colmajor, hipStream_t st) {
+  if (dtype == SPLAT_BF16)
+    return launched(splat::launch_rspmm_tiles(h->dev, B * H, d, P, V, O, out_dtype, colmajor, st),
+                    "rspmm");
+  return launched(
+      splat::launch_rspmm_rows(h->dev, dtype, B * H, d, P, V, O, out_dtype, colmajor, st), "rspmm");
+}
+
+splat_status launch_rsddmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                           const void* Q, const void* K, float scale, float* S, hipStream_t st) {
+  if (dtype == SPLAT_BF16)
+    return launched(splat::launch_rsddmm_tiles(h->dev, B * H, d, Q, K, scale, S, st), "rsddmm");
+  return launched(splat::launch_rsddmm_rows(h->dev, dtype, B * H, d, Q, K, scale, S, st), "rsddmm");
+}
+
+bool overlap(const float* a, const float* b, size_t n) {
+  const char *x = (const char*)a, *y = (const char*)b;
+  const size_t bytes = n * sizeof(float);
+  return x < y + bytes && y < x + bytes;
+}
+
+splat_status check_transpose(splat_acsr_t h, int32_t B, int32_t H, const float* P, const float* Pt) {
+  CHECK(check_handle(h, B, H));
+  CHECK(check_columns(h));
+  if (h->host.nnz == 0) return SPLAT_OK;
+  CHECK(check_ptr(P, "P"));
+  CHECK(check_ptr(Pt, "Pt"));
+  if (overlap(P, Pt, (size_t)B * H * h->host.nnz))
+    return fail(SPLAT_ERR_INVALID_ARG, "P and Pt must not overlap");
+  CHECK(check_tile_grid(h, B, H));
+  return SPLAT_OK;
+}
 
 }  // namespace
 
@@ -207,7 +270,8 @@ splat_status splat_pattern_full(int32_t L, splat_pattern_desc* out) {
 
 splat_status splat_acsr_build_ex(const splat_pattern_desc* desc, uint32_t flags, splat_acsr_t* out) {
   if (!desc || !out) return fail(SPLAT_ERR_INVALID_ARG, "desc and out must be non-NULL");
-  if (flags & ~SPLAT_PLAN_NO_SPAN) return fail(SPLAT_ERR_INVALID_ARG, "unknown plan flags 0x%x", flags);
+  if (flags & ~(SPLAT_PLAN_NO_SPAN | SPLAT_PLAN_COLUMNS))
+    return fail(SPLAT_ERR_INVALID_ARG, "unknown plan flags 0x%x", flags);
   if ((flags & SPLAT_PLAN_NO_SPAN) && desc->L > SPLAT_NO_SPAN_MAX_L)
     return fail(SPLAT_ERR_UNSUPPORTED, "SPLAT_PLAN_NO_SPAN needs L <= %d, got %d", SPLAT_NO_SPAN_MAX_L,
                 desc->L);
@@ -265,6 +329,21 @@ splat_status splat_acsr_info(splat_acsr_t h, splat_acsr_info_t* out) {
   out->n_full_tiles = a.n_full;
   out->nnz = a.nnz;
   out->computed = a.computed;
+  out->columns = a.col_regular;
+  return ok();
+}
+
+splat_status splat_acsr_export_csc(splat_acsr_t h, int32_t* col_ptr, int32_t* row_idx) {
+  if (!h || !col_ptr || (!row_idx && h->host.nnz > 0))
+    return fail(SPLAT_ERR_INVALID_ARG, "handle, col_ptr and row_idx must be non-NULL");
+  CHECK(check_columns(h));
+  const HostAcsr& a = h->host;
+  for (int32_t j = 0; j < a.L; ++j) {
+    const splat::ColRun& c = a.cols[j];
+    col_ptr[j] = c.ptr;
+    for (int32_t t = 0; t < c.count; ++t) row_idx[c.ptr + t] = c.start + c.stride * t;
+  }
+  col_ptr[a.L] = (int32_t)a.nnz;
   return ok();
 }
 
@@ -335,11 +414,8 @@ splat_status splat_rsddmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t 
   CHECK(check_ptr(K, "K"));
   if (h->host.nnz == 0) return ok();
   CHECK(check_ptr(S, "S"));
-  hipStream_t st = (hipStream_t)stream;
   if (dtype == SPLAT_BF16) CHECK(check_tile_grid(h, B, H));
-  if (dtype == SPLAT_BF16)
-    return launched(splat::launch_rsddmm_tiles(h->dev, B * H, d, Q, K, scale, S, st), "rsddmm");
-  return launched(splat::launch_rsddmm_rows(h->dev, dtype, B * H, d, Q, K, scale, S, st), "rsddmm");
+  return launch_rsddmm(h, dtype, B, H, d, Q, K, scale, S, (hipStream_t)stream);
 }
 
 splat_status splat_row_softmax(splat_acsr_t h, int32_t B, int32_t H, const float* S, float* P,
@@ -358,18 +434,23 @@ splat_status splat_row_softmax(splat_acsr_t h, int32_t B, int32_t H, const float
 
 splat_status splat_rspmm(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
                          const float* P, const void* V, void* O, splat_dtype out_dtype, void* stream) {
-  CHECK(check_handle(h, B, H));
-  CHECK(check_dtype(dtype, "dtype"));
-  CHECK(check_dtype(out_dtype, "out_dtype"));
-  CHECK(check_d(d));
-  if (h->host.nnz > 0) CHECK(check_ptr(P, "P"));
-  CHECK(check_ptr(V, "V"));
-  CHECK(check_ptr(O, "O"));
-  hipStream_t st = (hipStream_t)stream;
-  if (dtype == SPLAT_BF16) CHECK(check_tile_grid(h, B, H));
-  if (dtype == SPLAT_BF16)
-    return launched(splat::launch_rspmm_tiles(h->dev, B * H, d, P, V, O, out_dtype, st), "rspmm");
-  return launched(splat::launch_rspmm_rows(h->dev, dtype, B * H, d, P, V, O, out_dtype, st), "rspmm");
+  CHECK(check_rspmm(h, dtype, B, H, d, P, V, O, out_dtype, false));
+  return launch_rspmm(h, dtype, B, H, d, P, V, O, out_dtype, false, (hipStream_t)stream);
+}
+
+splat_status splat_rspmm_colmajor(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
+                                  const float* Pt, const void* V, void* O, splat_dtype out_dtype,
+                                  void* stream) {
+  CHECK(check_rspmm(h, dtype, B, H, d, Pt, V, O, out_dtype, true));
+  return launch_rspmm(h, dtype, B, H, d, Pt, V, O, out_dtype, true, (hipStream_t)stream);
+}
+
+splat_status splat_transpose_colmajor(splat_acsr_t h, int32_t B, int32_t H, const float* P, float* Pt,
+                                      void* stream) {
+  CHECK(check_transpose(h, B, H, P, Pt));
+  if (h->host.nnz == 0) return ok();
+  return launched(splat::launch_transpose_colmajor(h->dev, B * H, P, Pt, (hipStream_t)stream),
+                  "transpose_colmajor");
 }
 
 splat_status splat_sparse_mhsa_fwd(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H, int32_t d,
@@ -390,6 +471,35 @@ splat_status splat_sparse_mhsa_fwd(splat_acsr_t h, splat_dtype dtype, int32_t B,
                     "sparse_mhsa_fwd");
   return launched(splat::launch_fused_rows(h->dev, dtype, B * H, d, Q, K, V, scale, O, out_dtype, st),
                   "sparse_mhsa_fwd");
+}
+
+splat_status splat_sparse_mhsa_unfused(splat_acsr_t h, splat_dtype dtype, int32_t B, int32_t H,
+                                       int32_t d, const void* Q, const void* K, const void* V,
+                                       float scale, float* S, float* Pt, void* O,
+                                       splat_dtype out_dtype, float alpha, int32_t* used_colmajor,
+                                       void* stream) {
+  CHECK(check_handle(h, B, H));
+  const HostAcsr& a = h->host;
+  // the paper's density analysis: dense masks take the column-major layout
+  const double density = (double)a.nnz / ((double)a.L * (double)a.L);
+  const bool col = a.col_regular == 1 && a.nnz > 0 && density >= (double)alpha;
+  // every step is validated before anything is enqueued
+  CHECK(check_dtype(dtype, "dtype"));
+  CHECK(check_d(d));
+  CHECK(check_ptr(Q, "Q"));
+  CHECK(check_ptr(K, "K"));
+  CHECK(check_rspmm(h, dtype, B, H, d, S, V, O, out_dtype, false));
+  if (col) CHECK(check_transpose(h, B, H, S, Pt));
+  hipStream_t st = (hipStream_t)stream;
+  if (a.nnz > 0) {
+    CHECK(launch_rsddmm(h, dtype, B, H, d, Q, K, scale, S, st));
+    CHECK(launched(splat::launch_softmax(h->dev, B * H, S, S, st), "row_softmax"));
+    if (col)
+      CHECK(launched(splat::launch_transpose_colmajor(h->dev, B * H, S, Pt, st),
+                     "transpose_colmajor"));
+  }
+  if (used_colmajor) *used_colmajor = col ? 1 : 0;
+  return launch_rspmm(h, dtype, B, H, d, col ? Pt : S, V, O, out_dtype, col, st);
 }
 
 }  // extern "C"

@@ -76,13 +76,15 @@ __global__ __launch_bounds__(kWave) void k_rsddmm_rows(DevAcsr a, int d, const T
   }
 }
 
-template <typename T, typename OutT>
+// COL: P holds the head's values in column-major order, value (i, j) at
+// col_pos(cols[j], i).
+template <typename T, typename OutT, bool COL>
 __global__ __launch_bounds__(kWave) void k_rspmm_rows(DevAcsr a, int d, const float* __restrict__ P,
                                                       const T* __restrict__ V,
                                                       OutT* __restrict__ O) {
   const int i = blockIdx.x, bh = blockIdx.y, lane = threadIdx.x;
   const size_t head = (size_t)bh * a.L * d;
-  const float* p = P + (size_t)bh * a.nnz + a.row_ptr[i];
+  const float* p = P + (size_t)bh * a.nnz + (COL ? 0 : a.row_ptr[i]);
   const RowRuns rr = a.runs[i];
   const bool two = d > kWave;
   float acc0 = 0.f, acc1 = 0.f;
@@ -91,8 +93,9 @@ __global__ __launch_bounds__(kWave) void k_rspmm_rows(DevAcsr a, int d, const fl
     const Run q = rr.r[r];
 #pragma unroll 4
     for (int k = 0; k < q.count; ++k) {
-      const float pk = p[q.prefix + k];
-      const T* v = V + head + (size_t)(q.start + q.stride * k) * d;
+      const int j = q.start + q.stride * k;
+      const float pk = COL ? p[col_pos(a.cols[j], i)] : p[q.prefix + k];
+      const T* v = V + head + (size_t)j * d;
       acc0 = fmaf(pk, to_f32(v[lane]), acc0);
       if (two) acc1 = fmaf(pk, to_f32(v[lane + kWave]), acc1);
     }
@@ -168,23 +171,26 @@ hipError_t launch_rsddmm_rows(const DevAcsr& a, int dtype, int BH, int d, const 
   return hipGetLastError();
 }
 
-template <typename T>
+template <typename T, bool COL>
 static hipError_t rspmm_t(const DevAcsr& a, int BH, int d, const float* P, const void* V, void* O,
                           int out_dtype, hipStream_t st) {
   dim3 grid(a.L, BH);
   if (out_dtype == 0)
-    hipLaunchKernelGGL((k_rspmm_rows<T, float>), grid, dim3(kWave), 0, st, a, d, P, (const T*)V,
-                       (float*)O);
+    hipLaunchKernelGGL((k_rspmm_rows<T, float, COL>), grid, dim3(kWave), 0, st, a, d, P,
+                       (const T*)V, (float*)O);
   else
-    hipLaunchKernelGGL((k_rspmm_rows<T, __bf16>), grid, dim3(kWave), 0, st, a, d, P, (const T*)V,
-                       (__bf16*)O);
+    hipLaunchKernelGGL((k_rspmm_rows<T, __bf16, COL>), grid, dim3(kWave), 0, st, a, d, P,
+                       (const T*)V, (__bf16*)O);
   return hipGetLastError();
 }
 
 hipError_t launch_rspmm_rows(const DevAcsr& a, int dtype, int BH, int d, const float* P,
-                             const void* V, void* O, int out_dtype, hipStream_t st) {
-  return dtype == 0 ? rspmm_t<float>(a, BH, d, P, V, O, out_dtype, st)
-                    : rspmm_t<__bf16>(a, BH, d, P, V, O, out_dtype, st);
+                             const void* V, void* O, int out_dtype, bool colmajor, hipStream_t st) {
+  if (colmajor)
+    return dtype == 0 ? rspmm_t<float, true>(a, BH, d, P, V, O, out_dtype, st)
+                      : rspmm_t<__bf16, true>(a, BH, d, P, V, O, out_dtype, st);
+  return dtype == 0 ? rspmm_t<float, false>(a, BH, d, P, V, O, out_dtype, st)
+                    : rspmm_t<__bf16, false>(a, BH, d, P, V, O, out_dtype, st);
 }
 
 template <typename T>

@@ -339,15 +339,24 @@ __global__ __launch_bounds__(256) void k_softmax(const int32_t* __restrict__ row
 // part and a bf16 remainder (p - hi), each multiplied on the matrix cores:
 // P then enters with about 16 significant bits instead of 8, at the cost of
 // MFMA work this HBM-bound kernel has to spare.
-template <int D, typename OutT>
-__global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
+//
+// COL: P holds the values in the column-compressed, column-major layout
+// (section 9): the value of (row, key) is read at col_pos(cols[key], row),
+// with the tile's column descriptors staged in LDS beside its V rows.  The
+// same values enter the same MFMAs in the same order, so the result equals
+// the row-major kernel's.  At d = 128 its 32 scattered P loads per tile need
+// more than the 256 registers of two workgroups per CU, so it runs one.
+template <int D, typename OutT, bool COL>
+__global__ __launch_bounds__(kTileThreads, (COL && D == 128) ? 1 : 2) void k_rspmm_tiles(
     const Group* __restrict__ groups, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ row_ptr, const Tile* __restrict__ tiles,
-    const uint64_t* __restrict__ masks, int L, int BH, int64_t nnz, const float* __restrict__ P,
-    const __bf16* __restrict__ V, OutT* __restrict__ O) {
+    const uint64_t* __restrict__ masks, const ColRun* __restrict__ cols, int L, int BH,
+    int64_t nnz, const float* __restrict__ P, const __bf16* __restrict__ V,
+    OutT* __restrict__ O) {
   constexpr int RB = 2 * D, CPR = RB / 16, TB = kBN * RB, NDB = D / 32;
   constexpr int CPT = TB / 16 / kTileThreads;   // 16-byte chunks per thread and tile
   __shared__ __attribute__((aligned(16))) char vt[2][TB];
+  __shared__ ColRun ct[COL ? 2 : 1][COL ? kBN : 1];
 
   const int g = blockIdx.x / BH;
   const int bh = blockIdx.x - g * BH;
@@ -360,7 +369,7 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
   const int row = row_valid ? rows[grp.row_off + m] : 0;
   const size_t head = (size_t)bh * L * D;
   const __bf16* Vh = V + head;
-  const float* prow = P + (size_t)bh * nnz + row_ptr[row];
+  const float* prow = P + (size_t)bh * nnz + (COL ? 0 : row_ptr[row]);
 
   int voff[NDB];
   v_operand_offsets<D>(lane, voff);
@@ -388,16 +397,30 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
     }
   };
 
+  // column descriptors of a tile's keys (COL only): one per thread below nk
+  auto load_c = [&](const Tile& tl, ColRun& c) {
+    if (COL && tid < tl.nk) c = cols[tl.kb + tl.ks * tid];
+  };
+  auto store_c = [&](int slot, const Tile& tl, const ColRun& c) {
+    if (COL && tid < tl.nk) ct[slot][tid] = c;
+  };
+
   const int tb = grp.tile_begin, nt = grp.tile_end - grp.tile_begin;
   int cnt = 0;
   if (nt > 0) {
     u32x4_t vreg[CPT];
+    ColRun creg{0, 1, 0, 0};
     load_v(tiles[tb], vreg);
+    load_c(tiles[tb], creg);
     store_v(vt[0], vreg);
+    store_c(0, tiles[tb], creg);
     __syncthreads();
     for (int i = 0; i < nt; ++i) {
       const Tile tl = tiles[tb + i];
-      if (i + 1 < nt) load_v(tiles[tb + i + 1], vreg);
+      if (i + 1 < nt) {
+        load_v(tiles[tb + i + 1], vreg);
+        load_c(tiles[tb + i + 1], creg);
+      }
       const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
       if (wst != kWaveEmpty) {
         const uint64_t bits =
@@ -405,7 +428,16 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
         // P^T operand: k-step j, element e of lane half h is key
         // u = 16*j + 8*(e/4) + 4*h + e%4
         float pv[4][8];
-        if (row_valid) {
+        if (COL && row_valid) {
+          const ColRun* cc = ct[COL ? (i & 1) : 0];
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int u = 16 * j + 8 * (e >> 2) + 4 * h + (e & 3);
+              pv[j][e] = ((bits >> u) & 1ull) ? prow[col_pos(cc[u], row)] : 0.f;
+            }
+        } else if (row_valid) {
           const float* src = prow + cnt;
           if (wst == kWaveFull) {
 #pragma unroll
@@ -449,7 +481,10 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
             oacc[b] = mfma32(va[b][j], plo[j], oacc[b]);
           }
       }
-      if (i + 1 < nt) store_v(vt[(i + 1) & 1], vreg);
+      if (i + 1 < nt) {
+        store_v(vt[(i + 1) & 1], vreg);
+        store_c((i + 1) & 1, tiles[tb + i + 1], creg);
+      }
       __syncthreads();
     }
   }
@@ -462,6 +497,66 @@ __global__ __launch_bounds__(kTileThreads, 2) void k_rspmm_tiles(
       for (int rg = 0; rg < 4; ++rg)
         store4<OutT>(orow + b * 32 + rg * 8 + 4 * h, oacc[b][4 * rg], oacc[b][4 * rg + 1],
                      oacc[b][4 * rg + 2], oacc[b][4 * rg + 3]);
+  }
+}
+
+// Column-major copy of P (data-layout reordering, section 9).  One workgroup
+// per (row group, batch*head) walks the group's tiles as R-SpMM does; lane
+// (row m, half h) moves its row's values for keys 32h .. 32h+31 of each tile.
+// All lanes step through the keys together, so at each step the 32 lanes of
+// a half store one column at their rows' positions: consecutive rows of a
+// column land at consecutive addresses.
+__global__ __launch_bounds__(kTileThreads) void k_colmajor_tiles(
+    const Group* __restrict__ groups, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ row_ptr, const Tile* __restrict__ tiles,
+    const uint64_t* __restrict__ masks, const ColRun* __restrict__ cols, int BH, int64_t nnz,
+    const float* __restrict__ P, float* __restrict__ Pt) {
+  __shared__ ColRun ct[kBN];
+  const int g = blockIdx.x / BH;
+  const int bh = blockIdx.x - g * BH;
+  const Group grp = groups[g];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int qi = lane & 31, h = lane >> 5;
+  const int m = wave * kWaveRows + qi;
+  const bool row_valid = m < grp.nrows;
+  const int row = row_valid ? rows[grp.row_off + m] : 0;
+  const float* prow = P + (size_t)bh * nnz + row_ptr[row];
+  float* dst = Pt + (size_t)bh * nnz;
+  int cnt = 0;
+  for (int t = grp.tile_begin; t < grp.tile_end; ++t) {
+    const Tile tl = tiles[t];
+    __syncthreads();   // every wavefront is done with the previous tile's descriptors
+    if (tid < tl.nk) ct[tid] = cols[tl.kb + tl.ks * tid];
+    __syncthreads();
+    const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
+    if (wst == kWaveEmpty) continue;
+    const uint64_t bits =
+        wst == kWaveFull ? ~0ull : masks[(size_t)max(tl.mask_block, 0) * kBM + m];
+    if (row_valid && wst == kWaveFull) {
+      // the row's 32 values for this half are contiguous: 16-byte loads
+      const float* src = prow + cnt + 32 * h;
+      float v[32];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const f32x4u_t x = *(const f32x4u_t*)(src + 4 * q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[4 * q + e] = x[e];
+      }
+#pragma unroll
+      for (int u = 0; u < 32; ++u) dst[col_pos(ct[32 * h + u], row)] = v[u];
+    } else if (row_valid) {
+      const unsigned hb = (unsigned)(bits >> (32 * h));
+      const float* src = prow + cnt + (h ? __builtin_popcount((unsigned)bits) : 0);
+      int k = 0;
+      for (int u = 0; u < 32; ++u) {
+        if ((hb >> u) & 1u) {
+          dst[col_pos(ct[32 * h + u], row)] = src[k];
+          ++k;
+        }
+      }
+    }
+    cnt += popc64(bits);
   }
 }
 
@@ -481,11 +576,11 @@ hipError_t softmax_seg_launch(const DevAcsr& a, int BH, const float* S, float* P
   return hipGetLastError();
 }
 
-template <int D, typename OutT>
+template <int D, typename OutT, bool COL>
 hipError_t rspmm_launch(const DevAcsr& a, int BH, const float* P, const void* V, void* O,
                         hipStream_t st) {
-  hipLaunchKernelGGL((k_rspmm_tiles<D, OutT>), dim3(a.n_groups * BH), dim3(kTileThreads), 0, st,
-                     a.groups, a.rows, a.row_ptr, a.tiles, a.masks, a.L, BH, a.nnz, P,
+  hipLaunchKernelGGL((k_rspmm_tiles<D, OutT, COL>), dim3(a.n_groups * BH), dim3(kTileThreads), 0,
+                     st, a.groups, a.rows, a.row_ptr, a.tiles, a.masks, a.cols, a.L, BH, a.nnz, P,
                      (const __bf16*)V, (OutT*)O);
   return hipGetLastError();
 }
@@ -519,13 +614,27 @@ hipError_t launch_softmax(const DevAcsr& a, int BH, const float* S, float* P, hi
   return softmax_launch<8>(a, BH, S, P, st);   // longer rows take the two-pass path
 }
 
-hipError_t launch_rspmm_tiles(const DevAcsr& a, int BH, int d, const float* P, const void* V,
-                              void* O, int out_dtype, hipStream_t st) {
+template <bool COL>
+static hipError_t rspmm_tiles_t(const DevAcsr& a, int BH, int d, const float* P, const void* V,
+                                void* O, int out_dtype, hipStream_t st) {
   if (d == 64)
-    return out_dtype == 0 ? rspmm_launch<64, float>(a, BH, P, V, O, st)
-                          : rspmm_launch<64, __bf16>(a, BH, P, V, O, st);
-  return out_dtype == 0 ? rspmm_launch<128, float>(a, BH, P, V, O, st)
-                        : rspmm_launch<128, __bf16>(a, BH, P, V, O, st);
+    return out_dtype == 0 ? rspmm_launch<64, float, COL>(a, BH, P, V, O, st)
+                          : rspmm_launch<64, __bf16, COL>(a, BH, P, V, O, st);
+  return out_dtype == 0 ? rspmm_launch<128, float, COL>(a, BH, P, V, O, st)
+                        : rspmm_launch<128, __bf16, COL>(a, BH, P, V, O, st);
+}
+
+hipError_t launch_rspmm_tiles(const DevAcsr& a, int BH, int d, const float* P, const void* V,
+                              void* O, int out_dtype, bool colmajor, hipStream_t st) {
+  return colmajor ? rspmm_tiles_t<true>(a, BH, d, P, V, O, out_dtype, st)
+                  : rspmm_tiles_t<false>(a, BH, d, P, V, O, out_dtype, st);
+}
+
+hipError_t launch_transpose_colmajor(const DevAcsr& a, int BH, const float* P, float* Pt,
+                                     hipStream_t st) {
+  hipLaunchKernelGGL(k_colmajor_tiles, dim3(a.n_groups * BH), dim3(kTileThreads), 0, st, a.groups,
+                     a.rows, a.row_ptr, a.tiles, a.masks, a.cols, BH, a.nnz, P, Pt);
+  return hipGetLastError();
 }
 
 }  // namespace splat

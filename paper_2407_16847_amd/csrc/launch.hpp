@@ -20,7 +20,16 @@ struct DevAcsr {
   const Group* groups;      // n_groups
   const Tile* tiles;
   const uint64_t* masks;    // kBM row masks per tile that has a PARTIAL wavefront
+  const ColRun* cols;       // L single-run column descriptors, or null (no column-major layout)
 };
+
+// Position of `row` in the column-major value array of one head, for a row
+// that is in column c: c.ptr + (row - c.start) / c.stride.  The quotient is
+// exact and below 2^16, so the float reciprocal (1 ulp) rounds back to it.
+__device__ __forceinline__ int col_pos(const ColRun& c, int row) {
+  const float t = (float)(row - c.start) * __builtin_amdgcn_rcpf((float)c.stride);
+  return c.ptr + (int)__builtin_rintf(t);
+}
 
 // Every launcher enqueues on `st` and returns the launch status.
 // dtype / out dtype: 0 = fp32, 1 = bf16.
@@ -28,8 +37,9 @@ struct DevAcsr {
 // Row-per-wave kernels: any d in {64, 128}, both dtypes.
 hipError_t launch_rsddmm_rows(const DevAcsr& a, int dtype, int BH, int d, const void* Q,
                               const void* K, float scale, float* S, hipStream_t st);
+// colmajor: P holds the column-major values (requires a.cols).
 hipError_t launch_rspmm_rows(const DevAcsr& a, int dtype, int BH, int d, const float* P,
-                             const void* V, void* O, int out_dtype, hipStream_t st);
+                             const void* V, void* O, int out_dtype, bool colmajor, hipStream_t st);
 hipError_t launch_fused_rows(const DevAcsr& a, int dtype, int BH, int d, const void* Q,
                              const void* K, const void* V, float scale, void* O, int out_dtype,
                              hipStream_t st);
@@ -38,7 +48,11 @@ hipError_t launch_fused_rows(const DevAcsr& a, int dtype, int BH, int d, const v
 hipError_t launch_rsddmm_tiles(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
                                float scale, float* S, hipStream_t st);
 hipError_t launch_rspmm_tiles(const DevAcsr& a, int BH, int d, const float* P, const void* V,
-                              void* O, int out_dtype, hipStream_t st);
+                              void* O, int out_dtype, bool colmajor, hipStream_t st);
+
+// Row-major (CSR order) values -> column-major values (requires a.cols).
+hipError_t launch_transpose_colmajor(const DevAcsr& a, int BH, const float* P, float* Pt,
+                                     hipStream_t st);
 
 // Row softmax, any row length (rows of up to 2048 values in registers).
 hipError_t launch_softmax(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st);

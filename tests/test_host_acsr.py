@@ -346,7 +346,7 @@ def test_no_span_plan(kind, params, L):
 def test_no_span_plan_arguments(lib):
     d = splat.Pattern.window(100, 3).desc
     h = ctypes.c_void_p()
-    assert lib.splat_acsr_build_ex(ctypes.byref(d), 2, ctypes.byref(h)) == 1
+    assert lib.splat_acsr_build_ex(ctypes.byref(d), 4, ctypes.byref(h)) == 1
     assert b"unknown plan flags" in lib.splat_last_error()
     big = splat.Pattern.window(splat.NO_SPAN_MAX_L + 1, 3).desc
     assert lib.splat_acsr_build_ex(ctypes.byref(big), splat.PLAN_NO_SPAN, ctypes.byref(h)) == 2
@@ -361,3 +361,47 @@ def test_no_span_plan_arguments(lib):
     assert c.info() == a.info()
     for x, y in zip(a.export_plan(), c.export_plan()):
         np.testing.assert_array_equal(x, y)
+
+
+# --------------------------------------------------------------------------
+# column-wise analysis and the column-major index set (section 5.2)
+@pytest.mark.parametrize("kind,params,L", [
+    ("window", {"w": 5}, 300), ("blocked", {"block": 16}, 250),
+    ("strided_local", {"local": 9, "stride": 13}, 220), ("dilated", {"w": 7, "dilation": 3}, 200),
+    ("window_global", {"w": 6, "n_global": 4}, 150), ("window_global", {"w": 200, "n_global": 4}, 150),
+    ("full", {}, 70)])
+def test_columns_analysis_and_csc_export(kind, params, L):
+    M = om.dense_mask(kind, params, L)
+    a = splat.Acsr(splat.Pattern.named(kind, params, L), columns=True)
+    # the oracle's column-wise verdict: every non-empty column has affine indices
+    regular = all(oacsr.affine_indices(np.nonzero(M[:, j])[0].tolist()) is not None
+                  for j in range(L) if M[:, j].any())
+    assert a.info()["columns"] == int(regular)
+    b = splat.Acsr(splat.Pattern.named(kind, params, L))
+    for x, y in zip(a.export(), b.export()):          # the row side is unchanged
+        np.testing.assert_array_equal(x, y)
+    if regular:
+        cp, ri = a.export_csc()
+        cp0, ri0 = om.csc(M)
+        np.testing.assert_array_equal(cp, cp0)
+        np.testing.assert_array_equal(ri, ri0)
+    else:
+        with pytest.raises(splat.SplatError) as e:
+            a.export_csc()
+        assert e.value.name == "NOT_REGULAR"
+
+
+def test_columns_flag_errors(lib):
+    a = splat.Acsr(splat.Pattern.window(64, 2))
+    assert a.info()["columns"] == -1
+    with pytest.raises(splat.SplatError) as e:
+        a.export_csc()
+    assert e.value.name == "INVALID_ARG"
+    h = ctypes.c_void_p()
+    d = splat.Pattern.window(64, 2).desc
+    assert lib.splat_acsr_build_ex(ctypes.byref(d), splat.PLAN_COLUMNS | 4, ctypes.byref(h)) == 1
+    both = splat.Acsr(splat.Pattern.window(100, 3), span=False, columns=True)
+    assert both.info()["columns"] == 1
+    _check_plan(both, om.dense_mask("window", {"w": 3}, 100), span=False)
+    with pytest.raises(ValueError):
+        splat.Acsr(mask=np.eye(4, dtype=np.uint8), columns=True)

@@ -280,3 +280,37 @@ def test_terms_mask_clamping_keeps_the_residue():
     keeps only columns congruent to -4 (mod 3), i.e. 2, 5, 8, ..."""
     M = om.terms_mask(12, [_term(0, 1, (0, 0, -4), (0, 0, 11), stride=3)])
     assert np.flatnonzero(M[0]).tolist() == [2, 5, 8, 11]
+
+
+# --------------------------------------------------------------------------
+# column-compressed, column-major order (section 5.2)
+def test_csc_hand_worked_example():
+    import json
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "colmajor_example.json")))
+    M = np.array(g["mask"], dtype=bool)
+    rp, ci = om.csr(M)
+    cp, ri = om.csc(M)
+    assert rp.tolist() == g["row_ptr"] and ci.tolist() == g["col_idx"]
+    assert cp.tolist() == g["col_ptr"] and ri.tolist() == g["row_idx"]
+    assert om.colmajor_source(M).tolist() == g["colmajor_source"]
+
+
+@pytest.mark.parametrize("kind,params,L", [
+    ("window", {"w": 3}, 40), ("blocked", {"block": 8}, 37), ("strided_local", {"local": 5, "stride": 7}, 50),
+    ("dilated", {"w": 4, "dilation": 3}, 45), ("window_global", {"w": 2, "n_global": 3}, 30)])
+def test_csc_properties(kind, params, L):
+    M = om.dense_mask(kind, params, L)
+    rp, ci = om.csr(M)
+    cp, ri = om.csc(M)
+    src = om.colmajor_source(M)
+    assert (np.diff(cp) == M.sum(axis=0)).all()
+    for j in range(L):
+        rows = ri[cp[j]:cp[j + 1]]
+        np.testing.assert_array_equal(rows, np.nonzero(M[:, j])[0])     # the column, ascending
+        for t, i in enumerate(rows):
+            k = src[cp[j] + t]                                          # its CSR slot
+            assert rp[i] <= k < rp[i + 1] and ci[k] == j
+    assert sorted(src.tolist()) == list(range(int(M.sum())))            # a permutation
+    # going through the transpose and back is the identity
+    back = om.colmajor_source(M.T)
+    np.testing.assert_array_equal(src[back], np.arange(int(M.sum())))
