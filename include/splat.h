@@ -234,6 +234,51 @@ splat_status splat_acsr_export_plan(splat_acsr_t h, int32_t* groups, int32_t* ro
 splat_status splat_acsr_tile_row_mask(splat_acsr_t h, int32_t tile, int32_t row, uint64_t* bits);
 
 /*
+ * splat_acsr_tiling -- thread-block arrangements of the mask under the SDDMM
+ * cost model of section 7 (a host-side diagnostic for the tiling ablation of
+ * section 10; the kernels run the row-group plan above).
+ *
+ * A thread-block of m x n threads with anchor t and stretch s computes the
+ * points t + (i*s, j*s), i < m, j < n (section 7.2).
+ * method SPLAT_TILING_POSET -- poset tiling (section 7.3, Algorithm 1): in
+ *   rounds, every uncovered point that no other uncovered point comes before
+ *   (row and column both <=) becomes an anchor, and the points its block
+ *   computes are removed, until the mask is covered.  stretch 0 selects the
+ *   stretch (section 7.3.1): 1 unless every non-empty row is one run of a
+ *   common stride X > 1, then the divisor of X of lowest cost (ties: fewer
+ *   blocks); stretch >= 1 fixes it.
+ * method SPLAT_TILING_GRID -- unstretched blocks at every multiple of
+ *   (m, n) whose block meets the mask (stretch must be 0 or 1).
+ * *out receives the arrangement's block count lambda, |P| = nnz, and the
+ * quantities of section 7.2: divergent threads (computed points outside the
+ * mask, blocks reaching past the matrix included), redundant threads
+ * (lambda*m*n - |P| - divergent), reuse |P| / (lambda*m*n), coalescing
+ * (mean 1/stretch) and cost lambda / coalescing, plus the stretch used and
+ * the number of rounds.  anchors (optional) receives the first
+ * min(anchor_capacity, lambda) anchors as (row, column) pairs in placement
+ * order.  INVALID_ARG for bad sizes (m, n in [1, 1024]; (m-1)*s and
+ * (n-1)*s at most L + 1024), UNSUPPORTED above L = SPLAT_TILING_MAX_L.
+ * Host only.
+ */
+#define SPLAT_TILING_POSET 0
+#define SPLAT_TILING_GRID 1
+#define SPLAT_TILING_MAX_L 8192
+typedef struct {
+  int64_t blocks;
+  int64_t points;
+  int64_t divergent;
+  int64_t redundant;
+  double reuse;
+  double coalesced;
+  double cost;
+  int32_t stretch;
+  int32_t iterations;
+} splat_tiling_stats_t;
+
+splat_status splat_acsr_tiling(splat_acsr_t h, int32_t method, int32_t m, int32_t n, int32_t stretch,
+                               splat_tiling_stats_t* out, int32_t* anchors, int64_t anchor_capacity);
+
+/*
  * splat_rsddmm -- regular SDDMM (Equation 1, section 7.4):
  *   S[b,h, row_ptr[i] + k] = scale * sum_c Q[b,h,i,c] * K[b,h,col(i,k),c]
  * for every row i and its k-th column col(i, k) in ascending order.

@@ -63,6 +63,15 @@ class AcsrInfo(ctypes.Structure):
                 ("columns", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class TilingStats(ctypes.Structure):
+    _fields_ = [("blocks", ctypes.c_int64), ("points", ctypes.c_int64), ("divergent", ctypes.c_int64),
+                ("redundant", ctypes.c_int64), ("reuse", ctypes.c_double),
+                ("coalesced", ctypes.c_double), ("cost", ctypes.c_double),
+                ("stretch", ctypes.c_int32), ("iterations", ctypes.c_int32)]
+
+
+TILING_METHODS = {"poset": 0, "grid": 1}
+
 _LIB: Optional[ctypes.CDLL] = None
 
 
@@ -102,6 +111,7 @@ def load() -> ctypes.CDLL:
         "splat_rspmm": [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp],
         "splat_sparse_mhsa_fwd": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, i32, vp],
         "splat_acsr_export_csc": [vp, vp, vp],
+        "splat_acsr_tiling": [vp, i32, i32, i32, i32, P(TilingStats), vp, i64],
         "splat_transpose_colmajor": [vp, i32, i32, vp, vp, vp],
         "splat_rspmm_colmajor": [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp],
         "splat_sparse_mhsa_unfused": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, i32, f32,
@@ -278,6 +288,23 @@ class Acsr:
         _check(self._lib.splat_acsr_export_csc(self.handle, cp.ctypes.data_as(ctypes.c_void_p),
                                                ri.ctypes.data_as(ctypes.c_void_p)))
         return cp, ri[: self.nnz]
+
+    def tiling(self, method: str = "poset", m: int = 32, n: int = 32, stretch: int = 0,
+               anchors: bool = False):
+        """Thread-block arrangement statistics under the cost model of
+        section 7 (dict); with anchors=True also the (row, col) anchors
+        [blocks, 2] in placement order."""
+        st = TilingStats()
+        _check(self._lib.splat_acsr_tiling(self.handle, TILING_METHODS[method], m, n, stretch,
+                                           ctypes.byref(st), None, 0))
+        out = {f: getattr(st, f) for f, _ in TilingStats._fields_}
+        if not anchors:
+            return out
+        buf = np.zeros((max(st.blocks, 1), 2), dtype=np.int32)
+        _check(self._lib.splat_acsr_tiling(self.handle, TILING_METHODS[method], m, n, stretch,
+                                           ctypes.byref(st), buf.ctypes.data_as(ctypes.c_void_p),
+                                           st.blocks))
+        return out, buf[: st.blocks]
 
     def row_runs(self, row: int):
         buf = np.zeros(3 * MAX_RUNS, dtype=np.int32)

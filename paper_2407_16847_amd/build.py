@@ -19,7 +19,7 @@ OUT = os.path.join(HERE, "libsplat.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["acsr_host.cpp", "api.hip", "kernels_rows.hip", "kernels_mfma.hip", "kernels_tiles.hip"]
+SOURCES = ["acsr_host.cpp", "tiling.cpp", "api.hip", "kernels_rows.hip", "kernels_mfma.hip", "kernels_tiles.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", "-Wno-unknown-pragmas"]
 # Packed fp32 instructions stay off: plain float code must not be turned into

@@ -2,6 +2,7 @@
 // ACSR handle lifetime (host analysis + one device upload) and kernel dispatch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -11,6 +12,7 @@
 #include "../../include/splat.h"
 #include "acsr_host.hpp"
 #include "launch.hpp"
+#include "tiling.hpp"
 
 using splat::DevAcsr;
 using splat::HostAcsr;
@@ -330,6 +332,37 @@ splat_status splat_acsr_info(splat_acsr_t h, splat_acsr_info_t* out) {
   out->nnz = a.nnz;
   out->computed = a.computed;
   out->columns = a.col_regular;
+  return ok();
+}
+
+splat_status splat_acsr_tiling(splat_acsr_t h, int32_t method, int32_t m, int32_t n, int32_t stretch,
+                               splat_tiling_stats_t* out, int32_t* anchors, int64_t anchor_capacity) {
+  if (!h || !out) return fail(SPLAT_ERR_INVALID_ARG, "handle and out must be non-NULL");
+  if (anchor_capacity < 0) return fail(SPLAT_ERR_INVALID_ARG, "anchor_capacity must be >= 0");
+  splat::TilingStats st;
+  std::vector<int32_t> anc;
+  std::string err;
+  splat_status s;
+  try {
+    s = splat::tile_mask(h->host, method, m, n, stretch, anchors ? &anc : nullptr, st, err);
+  } catch (const std::bad_alloc&) {
+    s = SPLAT_ERR_OOM;
+    err = "host allocation failed during tiling";
+  }
+  if (s != SPLAT_OK) return fail(s, "%s", err.c_str());
+  out->blocks = st.blocks;
+  out->points = st.points;
+  out->divergent = st.divergent;
+  out->redundant = st.redundant;
+  out->reuse = st.reuse;
+  out->coalesced = st.coalesced;
+  out->cost = st.cost;
+  out->stretch = st.stretch;
+  out->iterations = st.iterations;
+  if (anchors) {
+    const int64_t k = std::min<int64_t>(anchor_capacity, st.blocks);
+    std::memcpy(anchors, anc.data(), sizeof(int32_t) * 2 * (size_t)k);
+  }
   return ok();
 }
 

@@ -1,0 +1,87 @@
+"""Host side: splat_acsr_tiling (poset and grid arrangements, section 7)
+against the tiling oracle -- the same anchors in the same order and the same
+cost-model quantities (integers exactly, ratios to the last bit)."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from oracle import masks as om
+from oracle import tiling as ot
+
+splat = pytest.importorskip("paper_2407_16847_amd")
+
+CASES = [
+    ("window", {"w": 3}, 40, 4, 4), ("window", {"w": 9}, 64, 8, 16),
+    ("blocked", {"block": 8}, 37, 4, 8), ("blocked", {"block": 16}, 64, 32, 32),
+    ("dilated", {"w": 4, "dilation": 3}, 48, 3, 3), ("dilated", {"w": 6, "dilation": 2}, 40, 4, 2),
+    ("strided_local", {"local": 5, "stride": 7}, 50, 4, 4),
+    ("window_global", {"w": 3, "n_global": 2}, 33, 4, 8), ("full", {}, 20, 8, 8),
+]
+
+
+def _check(got, want):
+    for k in ("blocks", "points", "divergent", "redundant", "stretch"):
+        assert got[k] == want[k], k
+    for k in ("reuse", "coalesced", "cost"):
+        assert got[k] == pytest.approx(want[k], rel=1e-15, abs=0), k
+
+
+@pytest.mark.parametrize("kind,params,L,m,n", CASES)
+def test_poset_matches_oracle(kind, params, L, m, n):
+    M = om.dense_mask(kind, params, L)
+    a = splat.Acsr(splat.Pattern.named(kind, params, L))
+    got, anchors = a.tiling("poset", m, n, anchors=True)
+    want_anchors, rounds, want = ot.poset_with_selection(M, m, n)
+    assert [tuple(x) for x in anchors.tolist()] == want_anchors
+    assert got["iterations"] == rounds
+    _check(got, want)
+    for s in (1, 2):                                  # fixed stretches
+        g, anc = a.tiling("poset", m, n, stretch=s, anchors=True)
+        wa, wr = ot.poset_tiling(ot.points_of(M), m, n, s)
+        assert [tuple(x) for x in anc.tolist()] == wa and g["iterations"] == wr
+        _check(g, ot.metrics(ot.points_of(M), wa, m, n, s))
+
+
+@pytest.mark.parametrize("kind,params,L,m,n", CASES)
+def test_grid_matches_oracle(kind, params, L, m, n):
+    M = om.dense_mask(kind, params, L)
+    a = splat.Acsr(splat.Pattern.named(kind, params, L))
+    got, anchors = a.tiling("grid", m, n, anchors=True)
+    P = ot.points_of(M)
+    want_anchors = ot.grid_tiling(P, L, m, n)
+    assert [tuple(x) for x in anchors.tolist()] == want_anchors
+    _check(got, ot.metrics(P, want_anchors, m, n, 1))
+
+
+def test_worked_example_through_the_library():
+    pts = [(0, 0), (0, 2), (1, 1), (1, 3), (2, 0), (2, 2), (3, 1), (3, 3)]
+    M = np.zeros((4, 4), dtype=np.uint8)
+    for x, y in pts:
+        M[x, y] = 1
+    a = splat.Acsr(mask=M)
+    st, anchors = a.tiling("poset", 2, 2, anchors=True)
+    assert st["stretch"] == 2 and anchors.tolist() == [[0, 0], [1, 1]] and st["reuse"] == 1.0
+
+
+def test_tiling_errors():
+    a = splat.Acsr(splat.Pattern.window(50, 2))
+    for args in (("poset", 0, 4), ("poset", 4, 2000), ("grid", 4, 4, 2)):
+        with pytest.raises(splat.SplatError) as e:
+            a.tiling(*args)
+        assert e.value.name == "INVALID_ARG"
+    with pytest.raises(splat.SplatError) as e:
+        a.tiling("poset", 64, 64, stretch=50)         # reaches past L + 1024
+    assert e.value.name == "INVALID_ARG"
+    big = splat.Acsr(splat.Pattern.window(8193, 1))
+    with pytest.raises(splat.SplatError) as e:
+        big.tiling("poset", 32, 32)
+    assert e.value.name == "UNSUPPORTED"
+    st = splat.TilingStats()
+    lib = splat.load()
+    assert lib.splat_acsr_tiling(a.handle, 7, 4, 4, 0, ctypes.byref(st), None, 0) == 1
+    # a short anchor buffer receives the first anchors only
+    full, anc = a.tiling("poset", 4, 4, anchors=True)
+    buf = (ctypes.c_int32 * 4)(-1, -1, -1, -1)
+    assert lib.splat_acsr_tiling(a.handle, 0, 4, 4, 0, ctypes.byref(st), buf, 2) == 0
+    assert list(buf) == anc[:2].reshape(-1).tolist()
