@@ -84,6 +84,48 @@ def cpu_baseline(w, Q, K, V, budget_s: float):
                       f"masked attention, {el:.1f} s"}
 
 
+def settle(fn, ms: float) -> int:
+    """Runs fn back to back for `ms` of wall time (synchronising every 32
+    calls so the queue stays short); returns the number of calls.  Untimed:
+    it only brings the GPU to its steady state under this load."""
+    import torch
+    n, t_end = 0, time.perf_counter() + ms / 1e3
+    while time.perf_counter() < t_end:
+        fn()
+        n += 1
+        if n % 32 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    return n
+
+
+def graph_replay_us(fn, reps: int) -> float:
+    """Per-call µs of `reps` calls captured into one HIP graph: median of 5
+    replays timed with events on the current stream."""
+    import statistics
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(3):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    times = []
+    for _ in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3 / reps)
+    return statistics.median(times[1:])
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -94,6 +136,11 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--settle-ms", type=float, default=300.0,
+                    help="untimed sustained run of the step before the warmup steps: the GPU "
+                         "reaches its steady clock only after some tens of ms under load")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the fused timings of the other synthetic workloads")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of known size (for counter scaling)")
     args = ap.parse_args()
@@ -127,6 +174,7 @@ def main() -> int:
     def step():
         splat.sparse_mhsa_fwd(acsr, Qd, Kd, Vd, w.scale, O=O)
 
+    settle_steps = settle(step, args.settle_ms)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -190,6 +238,30 @@ def main() -> int:
             y.copy_(x)
         torch.cuda.synchronize()
 
+    # the other synthetic workloads through the fused path, each as replays
+    # of 20 calls captured into one HIP graph (their kernels are short enough
+    # that the host cost of an eager call would dominate)
+    others = None
+    if not args.no_others:
+        others = []
+        for c in sorted(workloads.CONFIGS):
+            if c == args.config:
+                continue
+            wo = workloads.get(c)
+            Qo, Ko, Vo = (x.cuda() for x in workloads.make_qkv(wo))
+            ao = splat.Acsr(splat.Pattern.named(wo.kind, wo.params, wo.L))
+            Oo = torch.empty_like(Qo)
+            us = graph_replay_us(lambda: splat.sparse_mhsa_fwd(ao, Qo, Ko, Vo, wo.scale, O=Oo), 20)
+            tf = 4.0 * ao.nnz * wo.d * wo.B * wo.H / (us * 1e-6) / 1e12
+            others.append({"workload": wo.name, "dtype": wo.dtype, "us_per_call": round(us, 2),
+                           "TFLOPs": round(tf, 2),
+                           "pct_of_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)
+                           if wo.dtype == "bf16" else None,
+                           "kernel": f"k_fused_mfma<{wo.d}, bf16>" if wo.dtype == "bf16"
+                           else "k_fused_rows"})
+            ao.close()
+            del Qo, Ko, Vo, Oo
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, Q, K, V, args.cpu_seconds)
@@ -202,6 +274,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": {"ms": args.settle_ms, "steps": settle_steps},
         "ms_per_step": round(ms, 5),
         "higher_is_better": True,
         "scaling": "weak",
@@ -223,6 +296,7 @@ def main() -> int:
         "plan": {"groups": info["n_groups"], "tiles": info["n_tiles"], "full_tiles": info["n_full_tiles"],
                  "acsr_build_ms": round(build_ms, 2)},
         "unfused": unfused,
+        "other_workloads": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

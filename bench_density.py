@@ -142,6 +142,11 @@ def main() -> int:
                 return F.scaled_dot_product_attention(Q, K, V, attn_mask=bias, scale=scale)
         return dense_time(run, str(backend))
 
+    # bring the GPU to its steady clock before anything is timed (untimed)
+    from bench import settle
+    full = splat.Acsr(splat.Pattern.full(L))
+    settle(lambda: splat.sparse_mhsa_fwd(full, Q, K, V, scale, O=O), 300.0)
+    full.close()
     Pd = torch.softmax(torch.matmul(Q, Kt).float() * scale, dim=-1).to(torch.bfloat16)
     dense = {"flash_us": sdpa(SDPBackend.FLASH_ATTENTION),
              "qk_matmul_us": dense_time(lambda: torch.matmul(Q, Kt), "matmul Q K^T"),

@@ -100,7 +100,6 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 4 : 2) void k_rsddmm_tiles(
   }
   float* const Sh = S + (size_t)bh * nnz;
   const int roff = row_valid ? row_ptr[row] : 0;
-  float* srow = Sh + roff;
   int cnt = 0;
   __shared__ __attribute__((aligned(16))) float stage[kTileThreads / 64][kWaveRows * kStageStride];
   float* const stw = stage[wave];
@@ -153,13 +152,36 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 4 : 2) void k_rsddmm_tiles(
           __builtin_nontemporal_store(o, (f32x4u_t*)(Sh + off + 4 * cc));
         }
       }
-    } else if (row_valid) {
-      float* dst = srow + cnt;
-      {
+    } else {
+      // A row's present keys of the tile take consecutive places of S (their
+      // ranks), so the scores are compacted into the staging rows at their
+      // ranks and leave as row segments too, of popcount(bits) values each.
+      if (row_valid) {
         // key 8*g + 4*h + e is element 4*(g%4) + e of sacc[g/4]
         for_each_key(bits, h, [&](int g, int e, unsigned present, int pos) {
-          if (present) dst[pos] = sacc[g >> 2][4 * (g & 3) + e] * scale;
+          if (present) stw[qi * kStageStride + pos] = sacc[g >> 2][4 * (g & 3) + e] * scale;
         });
+      }
+      const int my_off = row_valid ? roff + cnt : -1;
+      const int my_n = row_valid ? popc64(bits) : 0;
+      const int rr = lane >> 4, cc = lane & 15;
+#pragma unroll
+      for (int it = 0; it < kWaveRows / 4; ++it) {
+        const int r = 4 * it + rr;
+        const int off = __shfl(my_off, r, 64);
+        const int n = __shfl(my_n, r, 64);
+        if (off >= 0 && 4 * cc < n) {
+          const float4 v = *(const float4*)(stw + r * kStageStride + 4 * cc);
+          if (4 * cc + 3 < n) {
+            const f32x4u_t o = {v.x, v.y, v.z, v.w};
+            __builtin_nontemporal_store(o, (f32x4u_t*)(Sh + off + 4 * cc));
+          } else {
+            float* d = Sh + off + 4 * cc;   // the row's last 1-3 values
+            d[0] = v.x;
+            if (4 * cc + 1 < n) d[1] = v.y;
+            if (4 * cc + 2 < n) d[2] = v.z;
+          }
+        }
       }
     }
     cnt += popc64(bits);
