@@ -79,9 +79,17 @@ def cpu_baseline(w, Q, K, V, budget_s: float):
             break
     el = time.perf_counter() - t0
     flops = 4.0 * nnz * w.d * heads
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:  # pragma: no cover
+        pass
     return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{heads} of {w.B * w.H} heads ({w.name}): brute-force mask + dense fp64 "
-                      f"masked attention, {el:.1f} s"}
+                      f"masked attention, {el:.1f} s",
+            "cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0)),
+            "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
 
 
 def settle(fn, ms: float) -> int:
@@ -178,6 +186,7 @@ def main() -> int:
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # the metric: K steps between two events
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(args.steps):
@@ -185,6 +194,18 @@ def main() -> int:
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
+    # a second pass of K steps with an event after each, for the spread of
+    # single-step times (the events themselves add a little to each step)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev[0].record(stream)
+    for k in range(args.steps):
+        step()
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    per_step = sorted(ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps))
+
+    def pct(q):
+        return round(per_step[min(len(per_step) - 1, int(q * len(per_step)))], 5)
 
     flops = 4.0 * nnz * w.d * w.B * w.H
     tflops = flops / (ms * 1e-3) / 1e12
@@ -276,6 +297,11 @@ def main() -> int:
         "warmup": args.warmup,
         "settle": {"ms": args.settle_ms, "steps": settle_steps},
         "ms_per_step": round(ms, 5),
+        "step_ms": {"median": pct(0.5), "p10": pct(0.1), "p90": pct(0.9),
+                    "pass": "a second pass of K steps, an event after each",
+                    "note": "no cache flush between steps: the inputs exceed the 32 MB of L2 but "
+                            "fit the 256 MB Infinity Cache; the fused kernel is bound by "
+                            "MFMA and VALU issue, not by memory"},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
