@@ -25,7 +25,10 @@ namespace {
 using namespace mfma;
 
 constexpr int kTileThreads = 256;   // 4 wavefronts x 32 rows of a group
-constexpr int kStageStride = 68;    // floats per staged score row: 64 + 4 against bank conflicts
+// A staged score row: up to 31 values carried from earlier tiles (before
+// kCarry), then the tile's 64; 100 floats keep rows 16-byte aligned.
+constexpr int kCarry = 32;
+constexpr int kStageStride = 100;
 
 // 4 floats at a 4-byte aligned address (values of a row start anywhere)
 typedef float f32x4u_t __attribute__((ext_vector_type(4), aligned(4)));
@@ -66,7 +69,7 @@ __device__ __forceinline__ void for_each_key(uint64_t bits, int h, F&& f) {
 // a store stream: occupancy (four wavefronts per SIMD for d = 64) is what
 // keeps enough of it in flight.
 template <int D>
-__global__ __launch_bounds__(kTileThreads, D == 64 ? 4 : 2) void k_rsddmm_tiles(
+__global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
     const Group* __restrict__ groups, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ row_ptr, const Tile* __restrict__ tiles,
     const uint64_t* __restrict__ masks, int L, int BH, int64_t nnz,
@@ -98,9 +101,14 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 4 : 2) void k_rsddmm_tiles(
       }
     }
   }
-  float* const Sh = S + (size_t)bh * nnz;
-  const int roff = row_valid ? row_ptr[row] : 0;
-  int cnt = 0;
+  // Positions are absolute float indices into S (S is 16-byte aligned), so
+  // that 16-byte chunks and 128-byte lines are those of the address space.
+  const int64_t sbase = (int64_t)((uintptr_t)S >> 2);
+  auto at = [&](int64_t a) { return S + (a - sbase); };   // the float at absolute index a
+  const int64_t row_start = row_valid ? sbase + (int64_t)bh * nnz + row_ptr[row] : 0;
+  const int row_len = row_valid ? row_ptr[row + 1] - row_ptr[row] : 0;
+  int cnt = 0;                 // the row's values produced so far
+  int64_t wr = row_start;      // the row's values written so far end here
   __shared__ __attribute__((aligned(16))) float stage[kTileThreads / 64][kWaveRows * kStageStride];
   float* const stw = stage[wave];
 
@@ -114,7 +122,9 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 4 : 2) void k_rsddmm_tiles(
       for (int ks = 0; ks < NKS; ++ks) ka[kb2][ks] = *(const bf16x8_t*)(krow + 16 * ks);
     }
   };
-  // One tile: this wavefront's scores of the tile, stored at their ranks.
+  // One tile: this wavefront's scores of the tile go to their staging rows
+  // (after the values a row still carries from earlier tiles), then every
+  // row writes the whole 128-byte lines it has completed.
   auto tile = [&](const Tile& tl, const bf16x8_t (&ka)[2][NKS]) {
     const int wst = (tl.flags >> (kWaveShift + 2 * wave)) & 3;
     if (wst == kWaveEmpty) return;
@@ -128,63 +138,65 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 4 : 2) void k_rsddmm_tiles(
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) sacc[kb2] = mfma32(ka[kb2][ks], qf[ks], sacc[kb2]);
     }
+    // A row's present keys of the tile take consecutive places of S (their
+    // ranks): staged at kCarry + rank.
     if (wst == kWaveFull) {
-      // scores into the staging rows, then out as row segments
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
           const float4 v = make_float4(sacc[kb2][4 * rg] * scale, sacc[kb2][4 * rg + 1] * scale,
                                        sacc[kb2][4 * rg + 2] * scale, sacc[kb2][4 * rg + 3] * scale);
-          *(float4*)(stw + qi * kStageStride + 32 * kb2 + 8 * rg + 4 * h) = v;
+          *(float4*)(stw + qi * kStageStride + kCarry + 32 * kb2 + 8 * rg + 4 * h) = v;
         }
-      const int my_off = row_valid ? roff + cnt : -1;   // this row's values of the tile
-      const int rr = lane >> 4, cc = lane & 15;
-#pragma unroll
-      for (int it = 0; it < kWaveRows / 4; ++it) {
-        const int r = 4 * it + rr;
-        const float4 v = *(const float4*)(stw + r * kStageStride + 4 * cc);
-        const int off = __shfl(my_off, r, 64);
-        if (off >= 0) {
-          // streamed out: S is far larger than the caches, and dirty S lines
-          // left there slow the kernel that reads S next
-          const f32x4u_t o = {v.x, v.y, v.z, v.w};
-          __builtin_nontemporal_store(o, (f32x4u_t*)(Sh + off + 4 * cc));
-        }
-      }
-    } else {
-      // A row's present keys of the tile take consecutive places of S (their
-      // ranks), so the scores are compacted into the staging rows at their
-      // ranks and leave as row segments too, of popcount(bits) values each.
-      if (row_valid) {
-        // key 8*g + 4*h + e is element 4*(g%4) + e of sacc[g/4]
-        for_each_key(bits, h, [&](int g, int e, unsigned present, int pos) {
-          if (present) stw[qi * kStageStride + pos] = sacc[g >> 2][4 * (g & 3) + e] * scale;
-        });
-      }
-      const int my_off = row_valid ? roff + cnt : -1;
-      const int my_n = row_valid ? popc64(bits) : 0;
-      const int rr = lane >> 4, cc = lane & 15;
-#pragma unroll
-      for (int it = 0; it < kWaveRows / 4; ++it) {
-        const int r = 4 * it + rr;
-        const int off = __shfl(my_off, r, 64);
-        const int n = __shfl(my_n, r, 64);
-        if (off >= 0 && 4 * cc < n) {
-          const float4 v = *(const float4*)(stw + r * kStageStride + 4 * cc);
-          if (4 * cc + 3 < n) {
-            const f32x4u_t o = {v.x, v.y, v.z, v.w};
-            __builtin_nontemporal_store(o, (f32x4u_t*)(Sh + off + 4 * cc));
-          } else {
-            float* d = Sh + off + 4 * cc;   // the row's last 1-3 values
-            d[0] = v.x;
-            if (4 * cc + 1 < n) d[1] = v.y;
-            if (4 * cc + 2 < n) d[2] = v.z;
-          }
-        }
-      }
+    } else if (row_valid) {
+      // key 8*g + 4*h + e is element 4*(g%4) + e of sacc[g/4]
+      for_each_key(bits, h, [&](int g, int e, unsigned present, int pos) {
+        if (present)
+          stw[qi * kStageStride + kCarry + pos] = sacc[g >> 2][4 * (g & 3) + e] * scale;
+      });
     }
-    cnt += popc64(bits);
+    // This row's staged values cover [wr, end): the carried part then the
+    // tile's.  Written now: up to the last line boundary, or to the row's
+    // end once the row is complete.
+    const int n = row_valid ? popc64(bits) : 0;
+    const int64_t start = row_start + cnt, end = start + n;
+    const int64_t line = end & ~(int64_t)31;
+    const int64_t new_wr = (cnt + n == row_len) ? end : (line > wr ? line : wr);
+    const int rr = lane >> 4, cc = lane & 15;
+#pragma unroll
+    for (int it = 0; it < kWaveRows / 4; ++it) {
+      const int r = 4 * it + rr;
+      const int64_t lo = __shfl(wr, r, 64), hi = __shfl(new_wr, r, 64);
+      const int64_t st = __shfl(start, r, 64), en = __shfl(end, r, 64);
+      const float* srow = stw + r * kStageStride + kCarry - st;   // srow[g]: value of index g
+      // 16-byte chunks from the chunk holding lo; at most (31 + 64) / 4 + 1 of them
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int64_t a = (lo & ~(int64_t)3) + 4 * (cc + 16 * k);
+        if (a >= hi) continue;
+        if (a >= lo && a + 4 <= hi) {
+          const f32x4u_t v = *(const f32x4u_t*)(srow + a);
+          __builtin_nontemporal_store(v, (f32x4u_t*)at(a));
+        } else {
+          // the row's first or last line: single values, cached so that the
+          // rest of the line (the neighbouring row's) merges with them
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (a + e >= lo && a + e < hi) *at(a + e) = srow[a + e];
+        }
+      }
+      // what is left of the row, [hi, en), moves to just before kCarry
+      const int left = (int)(en - hi);
+      float keep[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) keep[k] = (cc + 16 * k < left) ? srow[hi + cc + 16 * k] : 0.f;
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
+        if (cc + 16 * k < left) stw[r * kStageStride + kCarry - left + cc + 16 * k] = keep[k];
+    }
+    wr = new_wr;
+    cnt += n;
   };
   for (int t = grp.tile_begin; t < grp.tile_end; ++t) {
     const Tile tl = tiles[t];

@@ -393,6 +393,37 @@ def test_random_descriptor_patterns(gpu_lib, seed):
             assert np.abs(P[0, h] - Pref[0, h]).max() <= P_ABS
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_random_descriptor_patterns_large(gpu_lib, seed):
+    """Random patterns over many tiles and row groups (L = 1000 .. 3000), with
+    a ragged last group, against the dense oracle."""
+    splat = gpu_lib
+    rng = np.random.default_rng(5000 + seed)
+    L = int(rng.integers(1000, 3000))
+    d = 128 if seed % 2 else 64
+    dtype = "f32" if seed == 5 else "bf16"
+    for _ in range(20):     # redraw until every row fits the format's runs
+        terms = _random_terms(rng, L)
+        try:
+            a = splat.Acsr(splat.Pattern.from_terms(L, terms))
+            break
+        except splat.SplatError as e:
+            assert e.name == "UNSUPPORTED"
+    else:
+        pytest.fail("no buildable pattern in 20 draws")
+    print(f"[gpu] large random descriptor seed={seed} L={L} d={d} {dtype} terms={terms}", flush=True)
+    M = om.terms_mask(L, terms)
+    w = workloads.Workload("random_terms_large", 1, 2, L, d, dtype, ("terms", ()), 1.0, 6000 + seed)
+    Q, K, V = workloads.make_qkv(w)
+    ref = oa.masked_attention(Q, K, V, M, w.scale)
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.float32)
+    _, _, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
+    torch.cuda.synchronize()
+    check_O(O, ref, dtype, f"seed {seed} fused")
+    check_O(Ou, ref, dtype, f"seed {seed} unfused")
+
+
 # --------------------------------------------------------------------------
 # handles built by the paper's analysis pass on explicit masks (two-point
 # affine solve per row, regularity check), through both paths
