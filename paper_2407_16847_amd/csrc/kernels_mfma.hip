@@ -11,19 +11,26 @@
 //      16-byte chunks XOR-swizzled so the MFMA operand reads below are free of
 //      bank conflicts.  With 34 KiB of LDS and at most 128 VGPRs (d = 64),
 //      four workgroups share a CU: four wavefronts per SIMD to hide latency
-//   2. S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q^T stays in registers); in this
-//      orientation each lane holds 32 scores of ONE query, so the row max and
-//      row sum need one exchange with lane ^ 32 only
+//   2. S^T = K Q^T on v_mfma_f32_32x32x16_bf16, with Q^T held in registers and
+//      pre-scaled by scale*log2(e) (rounded to bf16), so the products are the
+//      scores in the log2 domain, t = s * scale*log2(e); in this orientation
+//      each lane holds 32 scores of ONE query, so row reductions need one
+//      exchange with lane ^ 32 only
 //   3. per wavefront (32 rows) the plan marks the tile EMPTY (skipped), FULL
 //      or PARTIAL; on PARTIAL tiles the scores outside each row's affine
 //      runs are set to -inf from the row's precomputed 64-bit tile mask
-//   4. online softmax in the log2 domain: p = exp2(s * scale*log2(e) - m);
-//      the running max m is only raised when a score exceeds it by more
-//      than 2^8 (so p <= 256 and O is rescaled rarely)
+//   4. online softmax against a per-row integer reference m: p = exp2(t - m).
+//      The fast pass computes exp2(t), rounds it toward zero to bf16 and
+//      applies 2^-m to each bf16 pair with one saturating 16-bit subtract
+//      from the exponent fields -- no per-score max, offset or multiply.  A
+//      slow pass redoes the tile from the exact row max when a row's tile sum
+//      exceeds 2^12 (the reference then rises to the next integer above the
+//      max and O is rescaled by a power of two), when a row has nothing
+//      accumulated yet and its sum is tiny, or when the reference lies
+//      outside [0, 100]
 //   5. O^T += V^T P^T on the same MFMA, P^T taken straight from the score
-//      registers (rounded toward zero to bf16 by one v_perm_b32 per pair; the
-//      row sum adds the same rounded values), V^T gathered by LDS transpose
-//      reads in the key order the score registers imply
+//      registers, V^T gathered by LDS transpose reads in the key order the
+//      score registers imply; the row sum adds the same rounded p
 //
 // At the end O = O^T / (row sum), written in the requested dtype.
 #include <hip/hip_runtime.h>
@@ -38,7 +45,10 @@ namespace {
 using namespace mfma;
 
 constexpr int kThreads = 256;           // 4 waves
-constexpr float kRescaleThreshold = 8.f; // log2 units
+constexpr float kSumLimit = 4096.f;   // largest tile row sum the fast pass accepts
+constexpr float kRefMax = 100.f;      // references the fast pass can apply, [0, kRefMax]
+constexpr float kRefLow = -100.f;     // row maxima below this keep their own reference
+constexpr float kFirstMin = 0x1p-60f; // smallest first tile sum the fast pass accepts
 
 template <int D>
 struct Geo {
@@ -85,17 +95,48 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
   }
 }
 
-// p = exp2(s * sl2 - m) for this lane's 32 scores, rounded toward zero to bf16
-// into the P^T operand (key order of the score registers); returns the sum
-// of the rounded values.
-__device__ __forceinline__ float tile_exp(const f32x16_t* s, float sl2, float neg_m,
-                                          bf16x8_t* pf) {
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+
+// Fast pass of one tile: p = exp2(t) * 2^-m for this lane's 32 scores t
+// (s * scale*log2(e), from the pre-scaled Q) and the row's integer reference
+// m >= 0.  exp2(t) is rounded toward zero to bf16 (one v_perm_b32 per pair);
+// the factor 2^-m is applied to each bf16 pair at once by subtracting m from
+// both exponent fields with unsigned saturation (msub = m*128 in each half),
+// which is exact for normal results and flushes results below 2^-126 to zero.
+// Returns the sum of the scaled values.
+__device__ __forceinline__ float tile_exp_fast(const f32x16_t* s, unsigned msub, bf16x8_t* pf) {
+  float l0 = 0.f, l1 = 0.f;
+  const u16x2_t sub = __builtin_bit_cast(u16x2_t, msub);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float e8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) e8[e] = exp2_hw(s[j >> 1][(j & 1) * 8 + e]);
+    bf16x2_t p2[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const u16x2_t raw = __builtin_bit_cast(u16x2_t, pack_bf16_rz(e8[2 * e], e8[2 * e + 1]));
+      p2[e] = __builtin_bit_cast(bf16x2_t, __builtin_elementwise_sub_sat(raw, sub));
+    }
+    pf[j] = __builtin_shufflevector(__builtin_shufflevector(p2[0], p2[1], 0, 1, 2, 3),
+                                    __builtin_shufflevector(p2[2], p2[3], 0, 1, 2, 3), 0, 1, 2, 3,
+                                    4, 5, 6, 7);
+    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[0], kOnes2, l0, false);
+    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[1], kOnes2, l1, false);
+    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[2], kOnes2, l0, false);
+    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[3], kOnes2, l1, false);
+  }
+  return l0 + l1;
+}
+
+// Slow pass: p = exp2(t - m) with the reference subtracted in fp32.
+__device__ __forceinline__ float tile_exp_ref(const f32x16_t* s, float m, bf16x8_t* pf) {
   float l0 = 0.f, l1 = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     float e8[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) e8[e] = exp2_hw(fmaf(s[j >> 1][(j & 1) * 8 + e], sl2, neg_m));
+    for (int e = 0; e < 8; ++e) e8[e] = exp2_hw(s[j >> 1][(j & 1) * 8 + e] - m);
     bf16x2_t p2[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) p2[e] = pack_bf16_rz(e8[2 * e], e8[2 * e + 1]);
@@ -110,41 +151,15 @@ __device__ __forceinline__ float tile_exp(const f32x16_t* s, float sl2, float ne
   return l0 + l1;
 }
 
-// Online-softmax step of one tile for this lane's row: optional mask, tile
-// max, lazy update of the running max (only when a score exceeds it by more
-// than 2^kRescaleThreshold), p = exp2(s * scale*log2(e) - m) into the P^T
-// operand and the running sum of the rounded p.  alpha is the factor the
-// output accumulator must be scaled by before this tile's P V is added; the
-// return value says whether any lane of the wavefront needs it.
-template <bool MASKED>
-__device__ __forceinline__ bool tile_softmax(f32x16_t* s, uint64_t mk, int h, float sl2,
-                                             float& m_run, float& l_run, float& alpha,
-                                             bf16x8_t* pf) {
-  if (MASKED) {
-    const uint64_t bits = mk >> (4 * h);
+// scores outside the row's affine runs in this tile set to -inf
+__device__ __forceinline__ void mask_scores(f32x16_t* s, uint64_t mk, int h) {
+  const uint64_t bits = mk >> (4 * h);
 #pragma unroll
-    for (int kb2 = 0; kb2 < 2; ++kb2) {
-      const unsigned word = (unsigned)(bits >> (32 * kb2));
+  for (int kb2 = 0; kb2 < 2; ++kb2) {
+    const unsigned word = (unsigned)(bits >> (32 * kb2));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb2][r] = keep_if_bit(s[kb2][r], word, 8 * (r >> 2) + (r & 3));
-    }
+    for (int r = 0; r < 16; ++r) s[kb2][r] = keep_if_bit(s[kb2][r], word, 8 * (r >> 2) + (r & 3));
   }
-  float mx0 = -INFINITY, mx1 = -INFINITY;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    mx0 = fmaxf(mx0, s[0][r]);
-    mx1 = fmaxf(mx1, s[1][r]);
-  }
-  float mx = fmaxf(mx0, mx1);
-  mx = fmaxf(mx, lane_xor32(mx));
-  const float m_new = fmaxf(m_run, mx * sl2);
-  const bool need = m_new > m_run + kRescaleThreshold;
-  alpha = need ? exp2_hw(m_run - m_new) : 1.f;   // exp2(-inf) = 0 on the first tile
-  m_run = need ? m_new : m_run;
-  l_run *= alpha;
-  const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
-  l_run += tile_exp(s, sl2, neg_m, pf);
-  return __any(need);
 }
 
 // The plan arrays are kernel arguments of their own, const and __restrict__,
@@ -180,7 +195,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       if (row_valid) {
-        qf[ks] = *(const bf16x8_t*)(qrow + ks * 16 + h * 8);
+        const bf16x8_t q = *(const bf16x8_t*)(qrow + ks * 16 + h * 8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[ks][e] = (__bf16)((float)q[e] * sl2);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) qf[ks][e] = (__bf16)0.f;
@@ -201,7 +218,13 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
   for (int b = 0; b < NDB; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[b][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  // the row's reference m (an integer; p = exp2(t - m)), the running sum of p
+  // and the reference as the fast pass applies it
+  // (l_run holds this lane's half of the row's keys; acc says whether the
+  // whole row has accumulated any weight, identical in both halves)
+  float m_run = 0.f, l_run = 0.f;
+  unsigned msub = 0u;
+  bool fast_ok = true, acc = false;
 
   const int tb = grp.tile_begin, nt = grp.tile_end - grp.tile_begin;
   if (nt > 0) {
@@ -244,21 +267,54 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
         };
         f32x16_t sacc[2];
         scores(sacc);
-        float alpha;
-        bf16x8_t pf[4];
-        bool need;
+        uint64_t mk = ~0ull;
         if (wst == kWavePartial) {
-          const uint64_t mk = *(const uint64_t*)(cur + 2 * G::TB + m * 8);
-          need = tile_softmax<true>(sacc, mk, h, sl2, m_run, l_run, alpha, pf);
-        } else {
-          need = tile_softmax<false>(sacc, 0, h, sl2, m_run, l_run, alpha, pf);
+          mk = *(const uint64_t*)(cur + 2 * G::TB + m * 8);
+          mask_scores(sacc, mk, h);
         }
-        if (need) {
+        bf16x8_t pf[4];
+        float lt = tile_exp_fast(sacc, msub, pf);
+        float lrow = lt + lane_xor32(lt);
+        // the slow pass takes the tile when, for some row, the fast pass
+        // cannot apply the reference, exceeds kSumLimit, or gives the row's
+        // first keys a total weight below kFirstMin (values that small may
+        // be fp32 subnormals, with too few bits left for bf16)
+        const bool redo = !fast_ok || !(lrow <= kSumLimit) ||
+                          (mk != 0 && lrow < kFirstMin && !acc);
+        if (__any(redo)) {
+          float mx0 = -INFINITY, mx1 = -INFINITY;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            mx0 = fmaxf(mx0, sacc[0][r]);
+            mx1 = fmaxf(mx1, sacc[1][r]);
+          }
+          float mx = fmaxf(mx0, mx1);
+          mx = fmaxf(mx, lane_xor32(mx));
+          // a row with nothing accumulated takes its reference from this
+          // tile; otherwise the reference only rises, to the next integer
+          // at or above the tile's max
+          float m_new = m_run;
+          if (!acc) {
+            if (mx > -INFINITY) m_new = mx < kRefLow ? ceilf(mx) : fmaxf(ceilf(mx), 0.f);
+          } else if (mx > m_run) {
+            m_new = ceilf(mx);
+          }
+          // a power of two, 1 if unchanged; a row with nothing accumulated
+          // has nothing to rescale (and its reference may fall)
+          const float alpha = acc ? exp2_hw(m_run - m_new) : 0.f;
+          lt = tile_exp_ref(sacc, m_new, pf);
+          lrow = lt + lane_xor32(lt);
+          l_run *= alpha;
+          m_run = m_new;
+          fast_ok = m_run >= 0.f && m_run <= kRefMax;
+          msub = fast_ok ? 0x00800080u * (unsigned)m_run : 0u;
 #pragma unroll
           for (int b = 0; b < NDB; ++b)
 #pragma unroll
             for (int r = 0; r < 16; ++r) oacc[b][r] *= alpha;
         }
+        l_run += lt;
+        acc = acc || lrow > 0.f;
         // O^T[d][query] += V^T[d][key] P^T[key][query]; k-step j, element e of
         // lane half h is key 16*j + 8*(e/4) + 4*h + e%4
         bf16x8_t va[NDB][4];

@@ -532,6 +532,49 @@ def test_bf16_launch_limit_is_an_error(gpu_lib):
     torch.cuda.synchronize()
 
 
+# Score regimes of the bf16 fused kernel's online softmax, one per head: the
+# reference rising over many tiles, scores far above and far below the range
+# its fast pass applies ([0, 100] in log2 units), and rows whose exponentials
+# start in the fp32 subnormal band.  q and k lie along one direction, so the
+# scores are set by their lengths; t = scale*log2(e)*q.k.
+REGIMES = {
+    "rising to ~280": (2.0, lambda c: 12.0 * c),
+    "near +400": (5.0, lambda c: 7.0 + 0 * c),
+    "near -400": (5.0, lambda c: -7.0 + 0 * c),
+    "near -120": (2.0, lambda c: -5.2 + 0 * c),
+    "falling from ~100 to -300": (2.0, lambda c: 4.3 - 17.3 * c),
+}
+
+
+@pytest.mark.parametrize("kind,params,L", [("window", {"w": 300}, 700),
+                                           ("window_global", {"w": 100, "n_global": 9}, 515)])
+def test_fused_score_regimes(gpu_lib, kind, params, L):
+    splat = gpu_lib
+    d, H = 64, len(REGIMES)
+    scale = 1.0 / math.sqrt(d)
+    g = torch.Generator().manual_seed(L)
+    u = torch.ones(d, dtype=torch.float64)
+    c = torch.arange(L, dtype=torch.float64) / L
+    Q = torch.empty(1, H, L, d, dtype=torch.float64)
+    K = torch.empty_like(Q)
+    for h, (qa, kf) in enumerate(REGIMES.values()):
+        Q[0, h] = qa * u + 0.05 * torch.randn(L, d, generator=g, dtype=torch.float64)
+        K[0, h] = kf(c)[:, None] * u + 0.3 * torch.randn(L, d, generator=g, dtype=torch.float64)
+    V = torch.randn(1, H, L, d, generator=g, dtype=torch.float64)
+    Q, K, V = (x.to(torch.bfloat16) for x in (Q, K, V))
+    print(f"[gpu] score regimes {kind} {params} L={L}", flush=True)
+    M = om.dense_mask(kind, params, L)
+    ref = oa.masked_attention(Q, K, V, M, scale)
+    a = splat.Acsr(splat.Pattern.named(kind, params, L))
+    Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
+    O = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, scale, out_dtype=torch.float32)
+    Ob = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, scale)
+    torch.cuda.synchronize()
+    for h, name in enumerate(REGIMES):
+        check_O(O[:, h:h + 1], ref[:, h:h + 1], "bf16", f"fused, {name}")
+        check_O(Ob[:, h:h + 1], ref[:, h:h + 1], "bf16", f"fused bf16 out, {name}")
+
+
 def test_many_heads(gpu_lib):
     """B*H = 600 (not a power of two): the workgroup -> (row group, head) split."""
     splat = gpu_lib
