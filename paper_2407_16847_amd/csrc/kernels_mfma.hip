@@ -20,14 +20,15 @@
 //      or PARTIAL; on PARTIAL tiles the scores outside each row's affine
 //      runs are set to -inf from the row's precomputed 64-bit tile mask
 //   4. online softmax against a per-row integer reference m: p = exp2(t - m).
-//      The fast pass computes exp2(t), rounds it toward zero to bf16 and
-//      applies 2^-m to each bf16 pair with one saturating 16-bit subtract
-//      from the exponent fields -- no per-score max, offset or multiply.  A
-//      slow pass redoes the tile from the exact row max when a row's tile sum
-//      exceeds 2^12 (the reference then rises to the next integer above the
-//      max and O is rescaled by a power of two), when a row has nothing
-//      accumulated yet and its sum is tiny, or when the reference lies
-//      outside [0, 100]
+//      The fast pass computes exp2(t), rounds it toward zero to bf16 and,
+//      only when some row has m > 0, applies 2^-m to each bf16 pair with one
+//      saturating 16-bit subtract from the exponent fields -- no per-score
+//      max, offset or multiply.  m stays 0 while a row's scores stay within
+//      2^6 of it.  A slow pass redoes the tile from the exact row max when a
+//      row's tile sum exceeds 2^12 (the reference then rises to the next
+//      integer above the max and O is rescaled by a power of two), when a
+//      row has nothing accumulated yet and its sum is tiny, or when the
+//      reference lies outside [0, 100]
 //   5. O^T += V^T P^T on the same MFMA, P^T taken straight from the score
 //      registers, V^T gathered by LDS transpose reads in the key order the
 //      score registers imply; the row sum adds the same rounded p
@@ -48,6 +49,8 @@ constexpr int kThreads = 256;           // 4 waves
 constexpr float kSumLimit = 4096.f;   // largest tile row sum the fast pass accepts
 constexpr float kRefMax = 100.f;      // references the fast pass can apply, [0, kRefMax]
 constexpr float kRefLow = -100.f;     // row maxima below this keep their own reference
+constexpr float kRefSlack = 6.f;      // a row keeps its reference while its max stays within
+                                      // this of it (p <= 2^6, a 64-key tile sum <= 2^12)
 constexpr float kFirstMin = 0x1p-60f; // smallest first tile sum the fast pass accepts
 
 template <int D>
@@ -95,18 +98,13 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
   }
 }
 
-typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
-
 // Fast pass of one tile: p = exp2(t) * 2^-m for this lane's 32 scores t
 // (s * scale*log2(e), from the pre-scaled Q) and the row's integer reference
-// m >= 0.  exp2(t) is rounded toward zero to bf16 (one v_perm_b32 per pair);
-// the factor 2^-m is applied to each bf16 pair at once by subtracting m from
-// both exponent fields with unsigned saturation (msub = m*128 in each half),
-// which is exact for normal results and flushes results below 2^-126 to zero.
-// Returns the sum of the scaled values.
-__device__ __forceinline__ float tile_exp_fast(const f32x16_t* s, unsigned msub, bf16x8_t* pf) {
+// m >= 0.  exp2(t) is rounded toward zero to bf16 (one v_perm_b32 per pair)
+// and summed; returns that sum.  The factor 2^-m is applied afterwards, by
+// scale_pairs, only when some row of the wavefront has m > 0.
+__device__ __forceinline__ float tile_exp_fast(const f32x16_t* s, bf16x8_t* pf) {
   float l0 = 0.f, l1 = 0.f;
-  const u16x2_t sub = __builtin_bit_cast(u16x2_t, msub);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     float e8[8];
@@ -114,10 +112,7 @@ __device__ __forceinline__ float tile_exp_fast(const f32x16_t* s, unsigned msub,
     for (int e = 0; e < 8; ++e) e8[e] = exp2_hw(s[j >> 1][(j & 1) * 8 + e]);
     bf16x2_t p2[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const u16x2_t raw = __builtin_bit_cast(u16x2_t, pack_bf16_rz(e8[2 * e], e8[2 * e + 1]));
-      p2[e] = __builtin_bit_cast(bf16x2_t, __builtin_elementwise_sub_sat(raw, sub));
-    }
+    for (int e = 0; e < 4; ++e) p2[e] = pack_bf16_rz(e8[2 * e], e8[2 * e + 1]);
     pf[j] = __builtin_shufflevector(__builtin_shufflevector(p2[0], p2[1], 0, 1, 2, 3),
                                     __builtin_shufflevector(p2[2], p2[3], 0, 1, 2, 3), 0, 1, 2, 3,
                                     4, 5, 6, 7);
@@ -127,6 +122,20 @@ __device__ __forceinline__ float tile_exp_fast(const f32x16_t* s, unsigned msub,
     l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[3], kOnes2, l1, false);
   }
   return l0 + l1;
+}
+
+// p * 2^-m on the bf16 P^T operand: m subtracted from both exponent fields of
+// each pair with unsigned saturation (msub = m*128 in each half), exact for
+// normal results, flushing results below 2^-126 to zero.
+__device__ __forceinline__ void scale_pairs(bf16x8_t* pf, unsigned msub) {
+  typedef unsigned short u16x8_t __attribute__((ext_vector_type(8)));
+  u16x8_t sub;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sub[e] = (unsigned short)((e & 1) ? msub >> 16 : msub);
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    pf[j] = __builtin_bit_cast(bf16x8_t, __builtin_elementwise_sub_sat(
+                                             __builtin_bit_cast(u16x8_t, pf[j]), sub));
 }
 
 // Slow pass: p = exp2(t - m) with the reference subtracted in fp32.
@@ -224,6 +233,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
   // whole row has accumulated any weight, identical in both halves)
   float m_run = 0.f, l_run = 0.f;
   unsigned msub = 0u;
+  float mscale = 1.f;
   bool fast_ok = true, acc = false;
 
   const int tb = grp.tile_begin, nt = grp.tile_end - grp.tile_begin;
@@ -273,7 +283,11 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
           mask_scores(sacc, mk, h);
         }
         bf16x8_t pf[4];
-        float lt = tile_exp_fast(sacc, msub, pf);
+        float lt = tile_exp_fast(sacc, pf);
+        if (__any(msub != 0u)) {
+          scale_pairs(pf, msub);
+          lt *= mscale;   // 2^-m: the sum of the scaled pairs, exactly
+        }
         float lrow = lt + lane_xor32(lt);
         // the slow pass takes the tile when, for some row, the fast pass
         // cannot apply the reference, exceeds kSumLimit, or gives the row's
@@ -295,8 +309,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
           // at or above the tile's max
           float m_new = m_run;
           if (!acc) {
-            if (mx > -INFINITY) m_new = mx < kRefLow ? ceilf(mx) : fmaxf(ceilf(mx), 0.f);
-          } else if (mx > m_run) {
+            if (mx > -INFINITY) m_new = (mx < kRefLow || mx > kRefSlack) ? ceilf(mx) : 0.f;
+          } else if (mx > m_run + kRefSlack) {
             m_new = ceilf(mx);
           }
           // a power of two, 1 if unchanged; a row with nothing accumulated
@@ -308,6 +322,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
           m_run = m_new;
           fast_ok = m_run >= 0.f && m_run <= kRefMax;
           msub = fast_ok ? 0x00800080u * (unsigned)m_run : 0u;
+          mscale = exp2_hw(-m_run);
 #pragma unroll
           for (int b = 0; b < NDB; ++b)
 #pragma unroll
