@@ -85,9 +85,12 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
     const int bk = wave + 4 * k;
     const int r = bk * G::RPB + lane / G::CPR;
     const int pos = lane % G::CPR;
+    // one 32-bit lane offset from the scalar base: the load adds them itself
+    // (no 64-bit vector address arithmetic)
     const unsigned row = (unsigned)(tl.ks * min(r, last)) * (2u * D);
-    dma16(kbase + row + 16u * (pos ^ swz_k(r)), slot + bk * kDmaBlock);
-    dma16(vbase + row + 16u * (pos ^ swz_v(r)), slot + G::TB + bk * kDmaBlock);
+    const unsigned ko = row + 16u * (pos ^ swz_k(r)), vo = row + 16u * (pos ^ swz_v(r));
+    dma16(kbase + ko, slot + bk * kDmaBlock);
+    dma16(vbase + vo, slot + G::TB + bk * kDmaBlock);
   }
   // row masks only for tiles with a PARTIAL wavefront (the others never read
   // them; the ring barrier waits for every outstanding load, so the count of
