@@ -66,7 +66,7 @@ __device__ __forceinline__ void for_each_key(uint64_t bits, int h, F&& f) {
 // wavefront LDS buffer and come back as row segments, so each store writes
 // 4 rows x 256 contiguous bytes (16 lanes per row) instead of 32 rows x 32
 // bytes; on PARTIAL tiles each present score is stored at its rank.  This is
-// a store stream: occupancy (four wavefronts per SIMD for d = 64) is what
+// a store stream: occupancy (three wavefronts per SIMD for d = 64) is what
 // keeps enough of it in flight.
 template <int D>
 __global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
@@ -101,14 +101,22 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
       }
     }
   }
-  // Positions are absolute float indices into S (S is 16-byte aligned), so
-  // that 16-byte chunks and 128-byte lines are those of the address space.
-  const int64_t sbase = (int64_t)((uintptr_t)S >> 2);
-  auto at = [&](int64_t a) { return S + (a - sbase); };   // the float at absolute index a
-  const int64_t row_start = row_valid ? sbase + (int64_t)bh * nnz + row_ptr[row] : 0;
+  // Positions within a row are 32-bit float indices counted from the start
+  // of the 128-byte line that holds the row's first value, so that 16-byte
+  // chunks and 128-byte lines of the index are those of the address space
+  // (S is 16-byte aligned): the row's values sit at [lead, lead + row_len)
+  // from its line base S + rline.
+  const int64_t sidx = row_valid ? (int64_t)bh * nnz + row_ptr[row] : 0;
+  const int lead = (int)((((uintptr_t)S >> 2) + (uint64_t)sidx) & 31u);
+  const int64_t rline = sidx - lead;
   const int row_len = row_valid ? row_ptr[row + 1] - row_ptr[row] : 0;
   int cnt = 0;                 // the row's values produced so far
-  int64_t wr = row_start;      // the row's values written so far end here
+  int wr = lead;               // the row's values written so far end here
+  // the write-out below serves rows 4*it + lane/16; their line bases, once
+  const int rr = lane >> 4, cc = lane & 15;
+  int64_t rl[kWaveRows / 4];
+#pragma unroll
+  for (int it = 0; it < kWaveRows / 4; ++it) rl[it] = __shfl(rline, 4 * it + rr, 64);
   __shared__ __attribute__((aligned(16))) float stage[kTileThreads / 64][kWaveRows * kStageStride];
   float* const stw = stage[wave];
 
@@ -160,34 +168,33 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
     // tile's.  Written now: up to the last line boundary, or to the row's
     // end once the row is complete.
     const int n = row_valid ? popc64(bits) : 0;
-    const int64_t start = row_start + cnt, end = start + n;
-    const int64_t line = end & ~(int64_t)31;
-    const int64_t new_wr = (cnt + n == row_len) ? end : (line > wr ? line : wr);
-    const int rr = lane >> 4, cc = lane & 15;
+    const int start = lead + cnt, end = start + n;
+    const int new_wr = (cnt + n == row_len) ? end : max(end & ~31, wr);
 #pragma unroll
     for (int it = 0; it < kWaveRows / 4; ++it) {
       const int r = 4 * it + rr;
-      const int64_t lo = __shfl(wr, r, 64), hi = __shfl(new_wr, r, 64);
-      const int64_t st = __shfl(start, r, 64), en = __shfl(end, r, 64);
-      const float* srow = stw + r * kStageStride + kCarry - st;   // srow[g]: value of index g
+      const int lo = __shfl(wr, r, 64), hi = __shfl(new_wr, r, 64);
+      const int st = __shfl(start, r, 64), en = __shfl(end, r, 64);
+      const float* srow = stw + r * kStageStride + kCarry - st;   // srow[g]: value at index g
+      float* const grow = S + rl[it];                              // the row's line base
       // 16-byte chunks from the chunk holding lo; at most (31 + 64) / 4 + 1 of them
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
-        const int64_t a = (lo & ~(int64_t)3) + 4 * (cc + 16 * k);
+        const int a = (lo & ~3) + 4 * (cc + 16 * k);
         if (a >= hi) continue;
         if (a >= lo && a + 4 <= hi) {
           const f32x4u_t v = *(const f32x4u_t*)(srow + a);
-          __builtin_nontemporal_store(v, (f32x4u_t*)at(a));
+          __builtin_nontemporal_store(v, (f32x4u_t*)(grow + a));
         } else {
           // the row's first or last line: single values, cached so that the
           // rest of the line (the neighbouring row's) merges with them
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (a + e >= lo && a + e < hi) *at(a + e) = srow[a + e];
+            if (a + e >= lo && a + e < hi) grow[a + e] = srow[a + e];
         }
       }
       // what is left of the row, [hi, en), moves to just before kCarry
-      const int left = (int)(en - hi);
+      const int left = en - hi;
       float keep[2];
 #pragma unroll
       for (int k = 0; k < 2; ++k) keep[k] = (cc + 16 * k < left) ? srow[hi + cc + 16 * k] : 0.f;
