@@ -546,14 +546,16 @@ REGIMES = {
 }
 
 
-@pytest.mark.parametrize("kind,params,L", [("window", {"w": 300}, 700),
-                                           ("window_global", {"w": 100, "n_global": 9}, 515)])
-def test_fused_score_regimes(gpu_lib, kind, params, L):
+@pytest.mark.parametrize("kind,params,L,d", [("window", {"w": 300}, 700, 64),
+                                             ("window_global", {"w": 100, "n_global": 9}, 515, 64),
+                                             ("window", {"w": 200}, 450, 128)])
+def test_fused_score_regimes(gpu_lib, kind, params, L, d):
     splat = gpu_lib
-    d, H = 64, len(REGIMES)
+    H = len(REGIMES)
     scale = 1.0 / math.sqrt(d)
     g = torch.Generator().manual_seed(L)
-    u = torch.ones(d, dtype=torch.float64)
+    # |u|^2 * scale = 8 at every d, so each regime keeps its score range
+    u = torch.full((d,), math.sqrt(8.0 / (scale * d)), dtype=torch.float64)
     c = torch.arange(L, dtype=torch.float64) / L
     Q = torch.empty(1, H, L, d, dtype=torch.float64)
     K = torch.empty_like(Q)
@@ -562,7 +564,7 @@ def test_fused_score_regimes(gpu_lib, kind, params, L):
         K[0, h] = kf(c)[:, None] * u + 0.3 * torch.randn(L, d, generator=g, dtype=torch.float64)
     V = torch.randn(1, H, L, d, generator=g, dtype=torch.float64)
     Q, K, V = (x.to(torch.bfloat16) for x in (Q, K, V))
-    print(f"[gpu] score regimes {kind} {params} L={L}", flush=True)
+    print(f"[gpu] score regimes {kind} {params} L={L} d={d}", flush=True)
     M = om.dense_mask(kind, params, L)
     ref = oa.masked_attention(Q, K, V, M, scale)
     a = splat.Acsr(splat.Pattern.named(kind, params, L))
