@@ -247,6 +247,13 @@ splat_status splat_acsr_tile_row_mask(splat_acsr_t h, int32_t tile, int32_t row,
  *   stretch (section 7.3.1): 1 unless every non-empty row is one run of a
  *   common stride X > 1, then the divisor of X of lowest cost (ties: fewer
  *   blocks); stretch >= 1 fixes it.
+ * method SPLAT_TILING_NAIVE -- Naive Tiling (Appendix C, the comparison
+ *   point of the SDDMM tiling ablation in section 10): the mask is cut into
+ *   patches of m consecutive rows (starting at row 0) and each patch is tiled
+ *   from left to right by unstretched blocks, the first at the patch's
+ *   leftmost point and the others n columns apart, ceil(w / n) of them for a
+ *   patch of width w (leftmost to rightmost point, inclusive); patches
+ *   without points take none (stretch must be 0 or 1).
  * method SPLAT_TILING_GRID -- unstretched blocks at every multiple of
  *   (m, n) whose block meets the mask (stretch must be 0 or 1).
  * *out receives the arrangement's block count lambda, |P| = nnz, and the
@@ -262,6 +269,7 @@ splat_status splat_acsr_tile_row_mask(splat_acsr_t h, int32_t tile, int32_t row,
  */
 #define SPLAT_TILING_POSET 0
 #define SPLAT_TILING_GRID 1
+#define SPLAT_TILING_NAIVE 2
 #define SPLAT_TILING_MAX_L 8192
 typedef struct {
   int64_t blocks;

@@ -28,8 +28,17 @@ reuse): in the section's worked example the stretched and the unstretched
 arrangements of a stride-2 mask cost the same, and the text presents the
 stretched one as the better.
 
-The grid arrangement (the comparison point) places unstretched blocks at
-every multiple of (m, n) whose block meets P.
+Naive Tiling (Appendix C, the comparison point of the SDDMM tiling ablation
+in section 10) cuts the mask into patches of m consecutive rows, starting at
+row 0, and tiles each patch from left to right with unstretched m x n blocks:
+the first block starts at the patch's leftmost point, the blocks follow each
+other n columns apart, and a patch of width w (leftmost to rightmost point,
+inclusive) takes ceil(w / n) of them.  Appendix C counts
+lambda_naive = sum over patches of ceil(w / n) and gives its closed form for
+structured dense polygons.
+
+The grid arrangement (a second, separately labelled comparison) places
+unstretched blocks at every multiple of (m, n) whose block meets P.
 """
 from __future__ import annotations
 
@@ -81,6 +90,28 @@ def poset_tiling(P: Set[Point], m: int, n: int, s: int):
             uncovered -= computed(a, m, n, s)
         rounds += 1
     return anchors, rounds
+
+
+def naive_tiling(P: Set[Point], L: int, m: int, n: int) -> List[Point]:
+    """Appendix C's Naive Tiling: anchors patch by patch (rows x0 = 0, m, 2m,
+    ...), left to right inside each patch."""
+    out = []
+    for x0 in range(0, L, m):
+        cols = [c for (r, c) in P if x0 <= r < x0 + m]
+        if not cols:
+            continue
+        left, right = min(cols), max(cols)
+        width = right - left + 1
+        for k in range(-(-width // n)):
+            out.append((x0, left + k * n))
+    return out
+
+
+def structured_polygon(r: int, h: int, l: int, lp: int) -> Set[Point]:
+    """Appendix C's structured dense polygon with parameters (r, l, h, l'):
+    r slabs of h rows; row y holds the l columns starting at floor(y/h)*l'.
+    Points as (row, column)."""
+    return {(y, (y // h) * lp + t) for y in range(r * h) for t in range(l)}
 
 
 def grid_tiling(P: Set[Point], L: int, m: int, n: int) -> List[Point]:

@@ -70,7 +70,7 @@ class TilingStats(ctypes.Structure):
                 ("stretch", ctypes.c_int32), ("iterations", ctypes.c_int32)]
 
 
-TILING_METHODS = {"poset": 0, "grid": 1}
+TILING_METHODS = {"poset": 0, "grid": 1, "naive": 2}
 
 _LIB: Optional[ctypes.CDLL] = None
 
@@ -347,6 +347,14 @@ def _dense(x: torch.Tensor, name: str, acsr: Acsr, d: Optional[int] = None):
     return x
 
 
+def _on(x: torch.Tensor, name: str, ref: torch.Tensor, shape=None) -> None:
+    """x lives on ref's device (and has `shape`, when given)."""
+    if x.device != ref.device:
+        raise ValueError(f"{name} is on {x.device}, expected {ref.device}")
+    if shape is not None and tuple(x.shape) != tuple(shape):
+        raise ValueError(f"{name} must be {tuple(shape)}, got {tuple(x.shape)}")
+
+
 def _stream() -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -366,10 +374,12 @@ def rsddmm(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, scale: float,
     _dense(K, "K", acsr, d)
     if K.dtype != Q.dtype or K.shape[:2] != Q.shape[:2]:
         raise ValueError("K must match Q in dtype, B and H")
+    _on(K, "K", Q)
     if S is None:
         S = torch.empty((B, H, acsr.nnz), dtype=torch.float32, device=Q.device)
-    elif S.dtype != torch.float32 or tuple(S.shape) != (B, H, acsr.nnz) or not S.is_contiguous():
-        raise ValueError(f"S must be a contiguous float32 [B, H, {acsr.nnz}] tensor")
+    else:
+        _values(S, "S", acsr, B, H)
+        _on(S, "S", Q)
     _check(load().splat_rsddmm(acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(),
                                float(scale), S.data_ptr() if S.numel() else None, _stream()))
     return S
@@ -377,15 +387,16 @@ def rsddmm(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, scale: float,
 
 def row_softmax(acsr: Acsr, S: torch.Tensor, P: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Softmax over each row's non-zeros; P may be S (in place)."""
+    if not isinstance(S, torch.Tensor) or not S.is_cuda:
+        raise TypeError("S must be a CUDA (HIP) tensor")
     if S.dtype != torch.float32 or S.dim() != 3 or S.shape[2] != acsr.nnz or not S.is_contiguous():
         raise ValueError(f"S must be a contiguous float32 [B, H, {acsr.nnz}] tensor")
-    if not S.is_cuda:
-        raise TypeError("S must be a CUDA (HIP) tensor")
     B, H, _ = S.shape
     if P is None:
         P = torch.empty_like(S)
-    elif P.dtype != torch.float32 or P.shape != S.shape or not P.is_contiguous():
-        raise ValueError("P must be a contiguous float32 tensor shaped like S")
+    else:
+        _values(P, "P", acsr, B, H)
+        _on(P, "P", S)
     _check(load().splat_row_softmax(acsr.handle, B, H, S.data_ptr() if S.numel() else None,
                                     P.data_ptr() if P.numel() else None, _stream()))
     return P
@@ -396,13 +407,14 @@ def rspmm(acsr: Acsr, P: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor
     """O = P V with P in ACSR (CSR) order."""
     _dense(V, "V", acsr)
     B, H, L, d = V.shape
-    if P.dtype != torch.float32 or tuple(P.shape) != (B, H, acsr.nnz) or not P.is_contiguous():
-        raise ValueError(f"P must be a contiguous float32 [B, H, {acsr.nnz}] tensor")
+    _values(P, "P", acsr, B, H)
+    _on(P, "P", V)
     odt = _out_dtype(out_dtype if O is None else O.dtype, V.dtype)
     if O is None:
         O = torch.empty((B, H, L, d), dtype=odt, device=V.device)
     else:
         _dense(O, "O", acsr, d)
+        _on(O, "O", V, (B, H, L, d))
     _check(load().splat_rspmm(acsr.handle, _DT[V.dtype], B, H, d, P.data_ptr() if P.numel() else None,
                               V.data_ptr(), O.data_ptr(), _DT[O.dtype], _stream()))
     return O
@@ -418,11 +430,13 @@ def sparse_mhsa_fwd(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, V: torch.Tenso
         _dense(x, n, acsr, d)
         if x.dtype != Q.dtype or x.shape[:2] != Q.shape[:2]:
             raise ValueError(f"{n} must match Q in dtype, B and H")
+        _on(x, n, Q)
     odt = _out_dtype(out_dtype if O is None else O.dtype, Q.dtype)
     if O is None:
         O = torch.empty((B, H, L, d), dtype=odt, device=Q.device)
     else:
         _dense(O, "O", acsr, d)
+        _on(O, "O", Q, (B, H, L, d))
     _check(load().splat_sparse_mhsa_fwd(acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(),
                                         V.data_ptr(), float(scale), O.data_ptr(), _DT[O.dtype],
                                         _stream()))
@@ -445,6 +459,7 @@ def transpose_colmajor(acsr: Acsr, P: torch.Tensor, Pt: Optional[torch.Tensor] =
     if Pt is None:
         Pt = torch.empty_like(P)
     _values(Pt, "Pt", acsr, B, H)
+    _on(Pt, "Pt", P)
     _check(load().splat_transpose_colmajor(acsr.handle, B, H, P.data_ptr() if P.numel() else None,
                                            Pt.data_ptr() if Pt.numel() else None, _stream()))
     return Pt
@@ -456,11 +471,13 @@ def rspmm_colmajor(acsr: Acsr, Pt: torch.Tensor, V: torch.Tensor, O: Optional[to
     _dense(V, "V", acsr)
     B, H, L, d = V.shape
     _values(Pt, "Pt", acsr, B, H)
+    _on(Pt, "Pt", V)
     odt = _out_dtype(out_dtype if O is None else O.dtype, V.dtype)
     if O is None:
         O = torch.empty((B, H, L, d), dtype=odt, device=V.device)
     else:
         _dense(O, "O", acsr, d)
+        _on(O, "O", V, (B, H, L, d))
     _check(load().splat_rspmm_colmajor(acsr.handle, _DT[V.dtype], B, H, d,
                                        Pt.data_ptr() if Pt.numel() else None, V.data_ptr(),
                                        O.data_ptr(), _DT[O.dtype], _stream()))
@@ -479,18 +496,22 @@ def sparse_mhsa_unfused(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, V: torch.T
         _dense(x, n, acsr, d)
         if x.dtype != Q.dtype or x.shape[:2] != Q.shape[:2]:
             raise ValueError(f"{n} must match Q in dtype, B and H")
+        _on(x, n, Q)
     if S is None:
         S = torch.empty((B, H, acsr.nnz), dtype=torch.float32, device=Q.device)
     _values(S, "S", acsr, B, H)
+    _on(S, "S", Q)
     if Pt is None and acsr.info()["columns"] == 1:
         Pt = torch.empty_like(S)
     if Pt is not None:
         _values(Pt, "Pt", acsr, B, H)
+        _on(Pt, "Pt", Q)
     odt = _out_dtype(out_dtype if O is None else O.dtype, Q.dtype)
     if O is None:
         O = torch.empty((B, H, L, d), dtype=odt, device=Q.device)
     else:
         _dense(O, "O", acsr, d)
+        _on(O, "O", Q, (B, H, L, d))
     used = ctypes.c_int32(-1)
     _check(load().splat_sparse_mhsa_unfused(
         acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(), V.data_ptr(), float(scale),

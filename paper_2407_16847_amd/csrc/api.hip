@@ -51,6 +51,9 @@ splat_status upload(splat_acsr* h) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(SPLAT_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  e = splat::prepare_fused_mfma();
+  if (e != hipSuccess)
+    return fail(SPLAT_ERR_HIP, "hipFuncSetAttribute (fused kernel LDS): %s", hipGetErrorString(e));
   const HostAcsr& a = h->host;
   auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t s_rowptr = al(sizeof(int32_t) * (a.L + 1));

@@ -364,16 +364,15 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
 }
 
 template <int D, typename OutT>
+hipError_t allow_lds() {
+  return hipFuncSetAttribute((const void*)k_fused_mfma<D, OutT>,
+                             hipFuncAttributeMaxDynamicSharedMemorySize, Geo<D>::LDS);
+}
+
+template <int D, typename OutT>
 hipError_t fused_launch(const DevAcsr& a, int BH, const void* Q, const void* K, const void* V,
                         float sl2, void* O, hipStream_t st) {
   constexpr int lds = Geo<D>::LDS;
-  static bool attr_set = false;   // the LDS size attribute is per kernel, set once
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute((const void*)k_fused_mfma<D, OutT>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
   hipLaunchKernelGGL((k_fused_mfma<D, OutT>), dim3(a.n_groups * BH), dim3(kThreads), lds, st,
                      a.groups, a.rows, a.tiles, a.masks, a.L, BH, (const __bf16*)Q,
                      (const __bf16*)K, (const __bf16*)V, sl2, (OutT*)O);
@@ -388,6 +387,14 @@ hipError_t fused_d(const DevAcsr& a, int BH, const void* Q, const void* K, const
 }
 
 }  // namespace
+
+hipError_t prepare_fused_mfma() {
+  hipError_t e = allow_lds<64, float>();
+  if (e == hipSuccess) e = allow_lds<64, __bf16>();
+  if (e == hipSuccess) e = allow_lds<128, float>();
+  if (e == hipSuccess) e = allow_lds<128, __bf16>();
+  return e;
+}
 
 hipError_t launch_fused_mfma(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
                              const void* V, float scale, void* O, int out_dtype, hipStream_t st) {

@@ -57,6 +57,11 @@ hipError_t launch_transpose_colmajor(const DevAcsr& a, int BH, const float* P, f
 // Row softmax, any row length (rows of up to 2048 values in registers).
 hipError_t launch_softmax(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st);
 
+// Allows the fused kernels their dynamic LDS (above the default limit at
+// d = 128) on the current device.  Called once per handle at build time, on
+// the handle's device, so launches never change kernel attributes.
+hipError_t prepare_fused_mfma();
+
 hipError_t launch_fused_mfma(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
                              const void* V, float scale, void* O, int out_dtype, hipStream_t st);
 

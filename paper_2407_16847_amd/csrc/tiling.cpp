@@ -6,11 +6,14 @@
 // points t + (i*s, j*s), i < m, j < n (section 7.2).  Poset tiling
 // (section 7.3) covers the mask's point set P in rounds: every round takes
 // the uncovered points that no other uncovered point comes before (x' <= x
-// and y' <= y) as new anchors and removes what their blocks compute.  The
-// grid arrangement places unstretched blocks at every multiple of (m, n)
-// whose block meets P.  For either arrangement the cost-model quantities of
-// section 7.2 are reported: divergent threads (computed points outside P),
-// redundant threads, reuse, coalescing (mean 1/stretch) and cost.
+// and y' <= y) as new anchors and removes what their blocks compute.  Naive
+// Tiling (Appendix C) cuts the mask into patches of m consecutive rows and
+// tiles each from its leftmost to its rightmost point with ceil(width / n)
+// unstretched blocks, n columns apart.  The grid arrangement places
+// unstretched blocks at every multiple of (m, n) whose block meets P.  For
+// every arrangement the cost-model quantities of section 7.2 are reported:
+// divergent threads (computed points outside P), redundant threads, reuse,
+// coalescing (mean 1/stretch) and cost.
 #include "tiling.hpp"
 
 #include <algorithm>
@@ -193,8 +196,41 @@ splat_status tile_mask(const HostAcsr& a, int32_t method, int32_t m, int32_t n, 
     st.iterations = 1;
     return SPLAT_OK;
   }
+  if (method == SPLAT_TILING_NAIVE) {
+    if (stretch > 1) {
+      err = "naive tiling is unstretched";
+      return SPLAT_ERR_INVALID_ARG;
+    }
+    Bitmap comp(a.L + m - 1, a.L + n - 1);
+    int64_t blocks = 0;
+    if (anchors) anchors->clear();
+    for (int32_t x = 0; x < a.L; x += m) {
+      // the patch's leftmost and rightmost points, from the rows' runs
+      int32_t left = a.L, right = -1;
+      for (int32_t i = x; i < std::min(a.L, x + m); ++i)
+        for (int r = 0; r < SPLAT_MAX_RUNS; ++r) {
+          const Run& q = a.runs[i].r[r];
+          if (q.count <= 0) continue;
+          left = std::min(left, q.start);
+          right = std::max(right, q.start + q.stride * (q.count - 1));
+        }
+      if (right < 0) continue;   // a patch without points takes no block
+      const int32_t nb = (right - left + n) / n;
+      for (int32_t k = 0; k < nb; ++k) {
+        place(x, left + k * n, m, n, 1, comp, nullptr);
+        ++blocks;
+        if (anchors) {
+          anchors->push_back(x);
+          anchors->push_back(left + k * n);
+        }
+      }
+    }
+    finish(comp, points, m, n, 1, blocks, st);
+    st.iterations = 1;
+    return SPLAT_OK;
+  }
   if (method != SPLAT_TILING_POSET) {
-    err = "method must be SPLAT_TILING_POSET or SPLAT_TILING_GRID";
+    err = "method must be SPLAT_TILING_POSET, SPLAT_TILING_GRID or SPLAT_TILING_NAIVE";
     return SPLAT_ERR_INVALID_ARG;
   }
   if (stretch >= 1) {

@@ -17,7 +17,7 @@ struct TilingStats {
   int32_t stretch = 1, iterations = 0;
 };
 
-// method: SPLAT_TILING_POSET or SPLAT_TILING_GRID; stretch 0 selects it
+// method: SPLAT_TILING_POSET, SPLAT_TILING_GRID or SPLAT_TILING_NAIVE; stretch 0 selects it
 // (poset only).  anchors (optional) receives (row, col) pairs in placement
 // order.
 splat_status tile_mask(const HostAcsr& a, int32_t method, int32_t m, int32_t n, int32_t stretch,

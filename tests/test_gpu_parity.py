@@ -12,9 +12,9 @@ Tolerances (stated by the target and derived in the comments):
     relative to |R_ij| or to its row);
     P elementwise <= 1e-5 (S error times P plus fp32 exp/divide rounding),
     every row of P sums to 1 within 1e-5.
-Sizes: the three small workloads at full size against the dense oracle; the
-two L = 4096 workloads at full size (the launch the benchmark times) on
-sampled rows, each computed by the per-row oracle.
+Sizes: every workload at full size against the dense oracle, the two
+L = 4096 workloads in the launch the benchmark times: every row of every head
+of O, and S and P on four whole heads.
 """
 import math
 
@@ -87,21 +87,6 @@ def _s_err_csr(x, ref, q, k, row_ptr, col_idx, scale):
     return worst
 
 
-def check_csr_rows(S, P, Sref, Pref, row_ptr, rows, what, q, k, cols, scale):
-    """S, P (numpy [nnz]) and reference lists, on the given rows; q, k fp64
-    [L, d] of the head, cols the rows' column lists."""
-    for t, i in enumerate(rows):
-        seg = slice(row_ptr[i], row_ptr[i + 1])
-        if row_ptr[i + 1] == row_ptr[i]:
-            continue
-        s, p = S[seg].astype(np.float64), P[seg].astype(np.float64)
-        es = _score_err(s, Sref[t], q[i], k[cols[t]], scale)
-        ep = np.abs(p - Pref[t]).max()
-        assert es <= S_REL, f"{what} row {i}: S rel error {es:.3e}"
-        assert ep <= P_ABS, f"{what} row {i}: P abs error {ep:.3e}"
-        assert abs(p.sum() - 1.0) <= 1e-5, f"{what} row {i}: P row sum {p.sum()}"
-
-
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("cfg", [1, 2, 3])
 def test_small_configs_full_oracle(gpu_lib, cfg):
@@ -141,12 +126,25 @@ def _sample_rows(L, extra, rng, n_random=40):
     return sorted(rows)
 
 
+def _s_err_dense(s_csr, ref_csr, q, k, mask, scale):
+    """_score_err over every score of one head at once: the magnitude
+    scale * sum_c |q_ic k_jc| is one dense product of |q| and |k|^T,
+    gathered at the mask in CSR order."""
+    mag = (scale * (np.abs(q) @ np.abs(k).T))[mask]
+    err = np.abs(np.asarray(s_csr, dtype=np.float64) - ref_csr)
+    zero = mag == 0
+    assert (err[zero] == 0).all(), "scores whose terms are all 0 must be exactly 0"
+    return float((err[~zero] / mag[~zero]).max()) if (~zero).any() else 0.0
+
+
 @pytest.mark.parametrize("cfg", [4, 5])
-def test_large_configs_sampled_rows(gpu_lib, cfg):
-    """Full size, the benchmark's launch (bf16 in; fp32 and bf16 out)."""
+def test_large_configs_every_row(gpu_lib, cfg):
+    """Full size, the benchmark's launch (bf16 in; fp32 and bf16 out): every
+    row of every head of the fused and the unfused output against the dense
+    fp64 oracle, and S and P element by element on four whole heads."""
     splat = gpu_lib
     w = workloads.get(cfg)
-    print(f"[gpu] cfg{cfg} {w.name} full size, sampled rows", flush=True)
+    print(f"[gpu] cfg{cfg} {w.name} full size, every row of every head", flush=True)
     Q, K, V = workloads.make_qkv(w)
     a = splat.Acsr(splat.Pattern.named(w.kind, w.params, w.L))
     Qd, Kd, Vd = _dev(Q), _dev(K), _dev(V)
@@ -154,29 +152,38 @@ def test_large_configs_sampled_rows(gpu_lib, cfg):
     O16 = splat.sparse_mhsa_fwd(a, Qd, Kd, Vd, w.scale, out_dtype=torch.bfloat16)
     S, P, Ou = unfused(a, splat, Qd, Kd, Vd, w.scale, torch.float32)
     torch.cuda.synchronize()
-    O32, O16, Ou = O32.cpu().numpy(), O16.float().cpu().numpy(), Ou.cpu().numpy()
-    assert np.isfinite(O32).all() and np.isfinite(O16).all() and np.isfinite(Ou).all()
-    row_ptr, _ = a.export()
-    rng = np.random.default_rng(cfg)
-    edges = [0, 1, 63, 64, 65, 127, 128, 129, 255, 256, 511, 512, 513, 576, 577, 1000, 2047, 2048,
-             w.L - 513, w.L - 512, w.L - 129, w.L - 128, w.L - 2, w.L - 1]
+    outs = {"fused32": O32.cpu().numpy(), "fused16": O16.float().cpu().numpy(),
+            "unfused": Ou.cpu().numpy()}
+    del O32, O16, Ou
+    M = om.dense_mask(w.kind, w.params, w.L)
     q, k, v = oa.to_f64(Q), oa.to_f64(K), oa.to_f64(V)
-    heads = sorted({(0, 0), (w.B - 1, w.H - 1)} | {(int(rng.integers(w.B)), int(rng.integers(w.H)))})
-    worst = {"fused32": 0.0, "fused16": 0.0, "unfused": 0.0}
-    Sn, Pn = None, None
-    for b, h in heads:
-        rows = _sample_rows(w.L, edges, rng)
-        cols = om.row_columns_fast(w.kind, w.params, w.L, rows)
-        Sr, Pr, Or = oa.attention_rows(q[b, h], k[b, h], v[b, h], rows, cols, w.scale)
-        for name, O in (("fused32", O32), ("fused16", O16), ("unfused", Ou)):
-            err = float(np.abs(O[b, h, rows] - Or).max())
-            worst[name] = max(worst[name], err)
-            assert err <= BF16_ABS, f"cfg{cfg} {name} head {(b, h)}: {err:.3e}"
-        Sbh = S[b, h].cpu().numpy()
-        Pbh = P[b, h].cpu().numpy()
-        check_csr_rows(Sbh, Pbh, Sr, Pr, row_ptr, rows, f"cfg{cfg} head {(b, h)}", q[b, h],
-                       k[b, h], cols, w.scale)
-    print(f"[gpu] cfg{cfg} worst abs errors {worst}", flush=True)
+    heads = [(0, 0), (0, w.H - 1), (w.B - 1, w.H // 2), (w.B - 1, w.H - 1)]
+    rp, _ = a.export()
+    worst = {name: 0.0 for name in outs}
+    worst.update(S=0.0, P=0.0, rowsum=0.0)
+    for b in range(w.B):
+        for h in range(w.H):
+            Sd, Pd, Or = oa.attention_head(q[b, h], k[b, h], v[b, h], M, w.scale)
+            for name, O in outs.items():
+                assert np.isfinite(O[b, h]).all(), f"cfg{cfg} {name} head {(b, h)}: non-finite"
+                err = float(np.abs(O[b, h].astype(np.float64) - Or).max())
+                worst[name] = max(worst[name], err)
+                assert err <= BF16_ABS, f"cfg{cfg} {name} head {(b, h)}: {err:.3e}"
+            if (b, h) in heads:
+                Sg = S[b, h].cpu().numpy()
+                Pg = P[b, h].cpu().numpy().astype(np.float64)
+                es = _s_err_dense(Sg, Sd[M], q[b, h], k[b, h], M, w.scale)
+                ep = float(np.abs(Pg - Pd[M]).max())
+                sums = np.add.reduceat(Pg, rp[:-1][np.diff(rp) > 0])
+                er = float(np.abs(sums - 1.0).max())
+                worst["S"], worst["P"] = max(worst["S"], es), max(worst["P"], ep)
+                worst["rowsum"] = max(worst["rowsum"], er)
+                assert es <= S_REL, f"cfg{cfg} head {(b, h)}: S rel error {es:.3e}"
+                assert ep <= P_ABS, f"cfg{cfg} head {(b, h)}: P abs error {ep:.3e}"
+                assert er <= 1e-5, f"cfg{cfg} head {(b, h)}: P row sum off by {er:.3e}"
+            del Sd, Pd
+    print(f"[gpu] cfg{cfg} max errors over all {w.B * w.H} heads: "
+          + ", ".join(f"{k} {v:.3e}" for k, v in worst.items()), flush=True)
 
 
 # --------------------------------------------------------------------------
@@ -333,6 +340,45 @@ def test_argument_errors(gpu_lib):
     assert rc == 1 and b"aligned" in lib.splat_last_error()
     info = a.info()
     assert info["on_device"] == 1 and info["device"] == torch.cuda.current_device()
+
+
+def test_binding_rejects_mismatched_tensors(gpu_lib):
+    """The binding checks every caller-supplied output and workspace against
+    Q/V's shape and device before anything is launched: an O of the wrong
+    batch or head count would otherwise be written past its end, and a host
+    tensor's pointer would reach a kernel."""
+    splat = gpu_lib
+    L, d = 128, 64
+    a = splat.Acsr(splat.Pattern.window(L, 4))
+    B, H = 2, 3
+    x = torch.randn((B, H, L, d), device="cuda").to(torch.bfloat16)
+    small = torch.zeros((1, 1, L, d), dtype=torch.float32, device="cuda")
+    S = splat.rsddmm(a, x, x, 0.1)
+    P = splat.row_softmax(a, S)
+    torch.cuda.synchronize()
+    before = small.clone()
+    with pytest.raises(ValueError):
+        splat.sparse_mhsa_fwd(a, x, x, x, 0.1, O=small)
+    with pytest.raises(ValueError):
+        splat.rspmm(a, P, x, O=small)
+    with pytest.raises(ValueError):
+        splat.sparse_mhsa_unfused(a, x, x, x, 0.1, O=small)
+    with pytest.raises(ValueError):
+        splat.rsddmm(a, x, x, 0.1, S=torch.empty((1, 1, a.nnz), device="cuda"))
+    with pytest.raises(ValueError):
+        splat.row_softmax(a, S, P=torch.empty((1, H, a.nnz), device="cuda"))
+    with pytest.raises(TypeError):
+        splat.rsddmm(a, x, x, 0.1, S=torch.empty((B, H, a.nnz)))
+    with pytest.raises(TypeError):
+        splat.row_softmax(a, S.cpu())
+    with pytest.raises(TypeError):
+        splat.row_softmax(a, S, P=torch.empty((B, H, a.nnz)))
+    with pytest.raises(TypeError):
+        splat.rspmm(a, P.cpu(), x)
+    with pytest.raises(TypeError):
+        splat.sparse_mhsa_fwd(a, x, x, x.cpu(), 0.1)
+    torch.cuda.synchronize()
+    assert torch.equal(small, before), "a rejected call wrote its output"
 
 
 # --------------------------------------------------------------------------

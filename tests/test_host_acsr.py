@@ -405,3 +405,45 @@ def test_columns_flag_errors(lib):
     _check_plan(both, om.dense_mask("window", {"w": 3}, 100), span=False)
     with pytest.raises(ValueError):
         splat.Acsr(mask=np.eye(4, dtype=np.uint8), columns=True)
+
+
+# --------------------------------------------------------------------------
+def _snapshot(a):
+    rp, ci = a.export()
+    groups, rows, tiles = a.export_plan()
+    return [rp, ci, np.asarray(groups), np.asarray(rows), np.asarray(tiles)]
+
+
+def test_concurrent_builds_match_serial_builds():
+    """Handles built, queried and destroyed from several host threads at once
+    (ctypes releases the GIL around each call) equal the same handles built
+    one after the other: the build keeps no shared mutable state."""
+    from concurrent.futures import ThreadPoolExecutor
+    cases = [("window", {"w": 16}, 256), ("blocked", {"block": 64}, 1024),
+             ("strided_local", {"local": 128, "stride": 128}, 2048),
+             ("dilated", {"w": 256, "dilation": 2}, 1200),
+             ("window_global", {"w": 512, "n_global": 64}, 4096),
+             ("window", {"w": 3}, 5), ("full", {}, 300)]
+    serial = []
+    for kind, params, L in cases:
+        a = splat.Acsr(splat.Pattern.named(kind, params, L))
+        serial.append(_snapshot(a))
+        a.close()
+
+    def work(k):
+        kind, params, L = cases[k % len(cases)]
+        out = None
+        for _ in range(3):
+            a = splat.Acsr(splat.Pattern.named(kind, params, L))
+            snap = _snapshot(a)
+            a.close()
+            if out is not None:
+                for x, y in zip(out, snap):
+                    np.testing.assert_array_equal(x, y)
+            out = snap
+        return k % len(cases), out
+
+    with ThreadPoolExecutor(max_workers=8) as ex:
+        for k, snap in ex.map(work, range(4 * len(cases))):
+            for x, y in zip(serial[k], snap):
+                np.testing.assert_array_equal(x, y)

@@ -1,4 +1,5 @@
-"""Host side: splat_acsr_tiling (poset and grid arrangements, section 7)
+"""Host side: splat_acsr_tiling (poset tiling, section 7; Naive Tiling,
+Appendix C; the grid arrangement)
 against the tiling oracle -- the same anchors in the same order and the same
 cost-model quantities (integers exactly, ratios to the last bit)."""
 import ctypes
@@ -54,6 +55,36 @@ def test_grid_matches_oracle(kind, params, L, m, n):
     _check(got, ot.metrics(P, want_anchors, m, n, 1))
 
 
+@pytest.mark.parametrize("kind,params,L,m,n", CASES + [
+    ("window", {"w": 0}, 33, 4, 4), ("window", {"w": 5}, 64, 16, 16),
+    ("strided_local", {"local": 3, "stride": 9}, 61, 5, 7)])
+def test_naive_matches_oracle(kind, params, L, m, n):
+    M = om.dense_mask(kind, params, L)
+    a = splat.Acsr(splat.Pattern.named(kind, params, L))
+    got, anchors = a.tiling("naive", m, n, anchors=True)
+    P = ot.points_of(M)
+    want_anchors = ot.naive_tiling(P, L, m, n)
+    assert [tuple(x) for x in anchors.tolist()] == want_anchors
+    _check(got, ot.metrics(P, want_anchors, m, n, 1))
+
+
+def test_naive_closed_form_through_the_library():
+    """Window masks at L = 1024 away from the clamped borders: each m-row
+    patch of a window of half-width w is 2w + m columns wide (Appendix C,
+    h = l' = 1, l = 2w + 1), so an interior patch takes ceil((2w + m) / n)
+    blocks; the two border patches are narrower by w columns on one side."""
+    L = 1024
+    for w, m, n in ((3, 16, 16), (40, 8, 32), (100, 32, 8), (0, 16, 16)):
+        a = splat.Acsr(splat.Pattern.window(L, w))
+        st = a.tiling("naive", m, n)
+        interior = (L // m - 2) * (-(-(2 * w + m) // n))
+        border = 2 * (-(-(w + m) // n)) if w < m else None
+        if border is not None:
+            assert st["blocks"] == interior + border, (w, m, n)
+        else:
+            assert st["blocks"] >= interior
+
+
 def test_worked_example_through_the_library():
     pts = [(0, 0), (0, 2), (1, 1), (1, 3), (2, 0), (2, 2), (3, 1), (3, 3)]
     M = np.zeros((4, 4), dtype=np.uint8)
@@ -66,7 +97,7 @@ def test_worked_example_through_the_library():
 
 def test_tiling_errors():
     a = splat.Acsr(splat.Pattern.window(50, 2))
-    for args in (("poset", 0, 4), ("poset", 4, 2000), ("grid", 4, 4, 2)):
+    for args in (("poset", 0, 4), ("poset", 4, 2000), ("grid", 4, 4, 2), ("naive", 4, 4, 2)):
         with pytest.raises(splat.SplatError) as e:
             a.tiling(*args)
         assert e.value.name == "INVALID_ARG"

@@ -75,3 +75,84 @@ def test_arrangement_definitions(kind, params, L, m, n):
     costs = {s: ot.metrics(P, ot.poset_tiling(P, m, n, s)[0], m, n, s)["cost"]
              for s in range(1, X + 1) if X % s == 0}
     assert met["cost"] == min(costs.values()) and X % met["stretch"] == 0
+
+
+# --------------------------------------------------------------------------
+# Naive Tiling (Appendix C) pinned by its closed form for structured dense
+# polygons, written out here case by case from the theorem's statement:
+# with kappa = gcd(m, h), m = tau_m * kappa, h = tau_h * kappa and
+# tau_m = alpha * tau_h + beta (0 <= beta < tau_h),
+#   beta == 0: (r / tau_m) * tau_h * ceil((l + (alpha - 1) l') / n)
+#   beta != 0: (r / tau_m) * ((beta - 1) ceil((l + (alpha + 1) l') / n)
+#                             + (tau_h - beta + 1) ceil((l + alpha l') / n))
+def _ceil(a, b):
+    return -(-a // b)
+
+
+def _lambda_naive_closed_form(r, l, h, lp, m, n):
+    from math import gcd
+    kappa = gcd(m, h)
+    tau_m, tau_h = m // kappa, h // kappa
+    alpha, beta = divmod(tau_m, tau_h)
+    assert r % tau_m == 0, "the theorem covers whole cross-sections of lcm(m, h) rows"
+    if beta == 0:
+        per = tau_h * _ceil(l + (alpha - 1) * lp, n)
+    else:
+        per = (beta - 1) * _ceil(l + (alpha + 1) * lp, n) + (tau_h - beta + 1) * _ceil(l + alpha * lp, n)
+    return (r // tau_m) * per
+
+
+# (r, l, h, l', m, n): window masks (h = l' = 1, l = 2w + 1), blocked masks
+# (h = l' = w, l = 2w) with m dividing h, h dividing m, and neither, and a
+# few other polygons; beta = 0, beta = 1 and beta > 1 all occur
+POLYGONS = [
+    (24, 7, 1, 1, 4, 4),      # window w = 3, beta = 0
+    (30, 9, 1, 1, 3, 5),      # window w = 4
+    (32, 5, 1, 1, 16, 16),    # window w = 2, one block per patch
+    (40, 17, 1, 1, 8, 3),     # window w = 8, narrow blocks
+    (6, 16, 8, 8, 4, 4),      # blocked w = 8, m < h (alpha = 0, beta = 1)
+    (6, 16, 8, 8, 12, 5),     # blocked, m > h, gcd 4 (alpha = 1, beta = 1)
+    (10, 16, 8, 8, 20, 6),    # blocked, alpha = 2, beta = 1
+    (6, 6, 3, 3, 2, 4),       # blocked w = 3, m = 2 (alpha = 0, beta = 2)
+    (10, 6, 3, 3, 5, 4),      # blocked w = 3, m = 5 (alpha = 1, beta = 2)
+    (15, 14, 7, 7, 3, 5),     # blocked w = 7, m = 3 (alpha = 0, beta = 3)
+    (12, 7, 2, 3, 3, 4),      # h = 2, l' = 3, l = 7
+    (9, 10, 4, 2, 6, 3),      # h = 4, l' = 2, l = 10
+]
+
+
+@pytest.mark.parametrize("r,l,h,lp,m,n", POLYGONS)
+def test_naive_tiling_closed_form(r, l, h, lp, m, n):
+    P = ot.structured_polygon(r, h, l, lp)
+    L = max(r * h, (r - 1) * lp + l)
+    anchors = ot.naive_tiling(P, L, m, n)
+    assert len(anchors) == _lambda_naive_closed_form(r, l, h, lp, m, n)
+    # it is an arrangement: every point is computed, anchors sit on patch rows
+    met = ot.metrics(P, anchors, m, n, 1)
+    assert met["blocks"] == len(anchors)
+    assert all(x % m == 0 for x, _ in anchors)
+
+
+def test_naive_tiling_one_block_off_fails_the_pin():
+    """The closed form separates a correct count from one that is one block
+    off in any patch: dropping or adding a block changes the count."""
+    r, l, h, lp, m, n = POLYGONS[1]
+    P = ot.structured_polygon(r, h, l, lp)
+    L = max(r * h, (r - 1) * lp + l)
+    want = _lambda_naive_closed_form(r, l, h, lp, m, n)
+    anchors = ot.naive_tiling(P, L, m, n)
+    assert len(anchors[:-1]) != want and len(anchors + [anchors[0]]) != want
+    # and a patch width off by one (tiling from one column right of the
+    # leftmost point) leaves points uncovered
+    shifted = [(x, y + 1) for x, y in anchors]
+    with pytest.raises(AssertionError):
+        ot.metrics(P, shifted, m, n, 1)
+
+
+def test_naive_tiling_hand_example():
+    """Window w = 1 on 6 rows, m = 2, n = 2: patch rows {0,1} cover columns
+    0..2 (2 blocks from column 0), {2,3} columns 1..4 (2 blocks from 1),
+    {4,5} columns 3..5 (2 blocks from 3)."""
+    M = om.dense_mask("window", {"w": 1}, 6)
+    P = ot.points_of(M)
+    assert ot.naive_tiling(P, 6, 2, 2) == [(0, 0), (0, 2), (2, 1), (2, 3), (4, 3), (4, 5)]
