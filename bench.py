@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 bf16 flop/clk x 2.4 GHz (MI355X dense)
 PEAK_HBM_GBS = 8000.0
+PEAK_F32_TFLOPS = 157.3     # dense fp32 (vector and matrix) for the fp32 workload
 
 
 def kernel_source_sha() -> str:
@@ -53,9 +54,11 @@ def load_traffic(workload: str) -> dict:
     return {k: v.get("traffic_bytes") for k, v in t.get("kernels", {}).items()}
 
 
-def cpu_baseline(w, Q, K, V, budget_s: float):
+def cpu_baseline(w, Q, K, V, budget_s: float, O_gpu=None):
     """The oracle as it stands on the host cores: whole heads (mask
-    enumeration + dense fp64 masked attention), as many as fit the budget."""
+    enumeration + dense fp64 masked attention), as many as fit the budget.
+    With the fused output O_gpu the heads the oracle computed also give the
+    largest elementwise error of the benchmarked launch (timed apart)."""
     import numpy as np
     from oracle import attention as oa
     from oracle import masks as om
@@ -70,9 +73,12 @@ def cpu_baseline(w, Q, K, V, budget_s: float):
     heads = 0
     import torch
     q, k, v = (x.to(dtype=torch.float32) for x in (Q, K, V))
+    refs = []
     while True:
         b, h = divmod(heads, w.H)
-        oa.attention_head(oa.to_f64(q[b, h]), oa.to_f64(k[b, h]), oa.to_f64(v[b, h]), M, w.scale)
+        _, _, o = oa.attention_head(oa.to_f64(q[b, h]), oa.to_f64(k[b, h]), oa.to_f64(v[b, h]), M,
+                                    w.scale)
+        refs.append(o)
         heads += 1
         el = time.perf_counter() - t0
         if el >= budget_s or heads == w.B * w.H or el * (heads + 1) / heads > 2.5 * budget_s:
@@ -85,11 +91,17 @@ def cpu_baseline(w, Q, K, V, budget_s: float):
             model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
     except OSError:  # pragma: no cover
         pass
+    err = None
+    if O_gpu is not None:
+        got = O_gpu.float().cpu().numpy().reshape(w.B * w.H, w.L, w.d)
+        err = {"max_abs_err": float(max(np.abs(got[t] - refs[t]).max() for t in range(heads))),
+               "bound": 2e-2, "heads_checked": heads,
+               "note": "fused output of the timed launch against the oracle's heads"}
     return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{heads} of {w.B * w.H} heads ({w.name}): brute-force mask + dense fp64 "
                       f"masked attention, {el:.1f} s",
             "cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0)),
-            "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
+            "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS"), "accuracy": err}
 
 
 def settle(fn, ms: float) -> int:
@@ -250,13 +262,45 @@ def main() -> int:
             unfused[name] = {"ms": round(t[k], 4), "algorithmic_bytes": alg[name],
                              "GBps": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4),
                              "traffic": traffic.get(name)}
+        # the column-compressed, column-major layout (section 9's layout
+        # switch) where every column of the mask is one affine run
+        ac = splat.Acsr(splat.Pattern.named(w.kind, w.params, w.L), columns=True)
+        if ac.info()["columns"] == 1:
+            Pt = torch.empty_like(P)
+            for _ in range(2):
+                splat.transpose_colmajor(ac, P, Pt)
+                splat.rspmm_colmajor(ac, Pt, Vd, O=Ou)
+            tc = [0.0, 0.0]
+            for _ in range(n_rep):
+                ev[0].record(stream)
+                splat.transpose_colmajor(ac, P, Pt)
+                ev[1].record(stream)
+                splat.rspmm_colmajor(ac, Pt, Vd, O=Ou)
+                ev[2].record(stream)
+                torch.cuda.synchronize()
+                for k in range(2):
+                    tc[k] += ev[k].elapsed_time(ev[k + 1])
+            colm = {"transpose_colmajor": 8 * E, "rspmm_colmajor": alg["rspmm"]}
+            unfused["colmajor"] = {}
+            for k, name in enumerate(colm):
+                tk = tc[k] / n_rep
+                gbs = colm[name] / (tk * 1e-3) / 1e9
+                unfused["colmajor"][name] = {"ms": round(tk, 4), "algorithmic_bytes": colm[name],
+                                             "GBps": round(gbs, 1),
+                                             "frac": round(gbs / PEAK_HBM_GBS, 4),
+                                             "traffic": traffic.get(name)}
+            del Pt
+        ac.close()
         del S, P, Ou
 
     if args.copy_calibration:
+        # an elementwise kernel that reads 256 MiB and writes 256 MiB (a
+        # device-to-device copy may run on a DMA engine, which the counters
+        # do not see)
         x = torch.empty(256 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda").fill_(1.0)
         y = torch.empty_like(x)
         for _ in range(3):
-            y.copy_(x)
+            torch.neg(x, out=y)
         torch.cuda.synchronize()
 
     # the other synthetic workloads through the fused path, each as replays
@@ -273,19 +317,35 @@ def main() -> int:
             ao = splat.Acsr(splat.Pattern.named(wo.kind, wo.params, wo.L))
             Oo = torch.empty_like(Qo)
             us = graph_replay_us(lambda: splat.sparse_mhsa_fwd(ao, Qo, Ko, Vo, wo.scale, O=Oo), 20)
-            tf = 4.0 * ao.nnz * wo.d * wo.B * wo.H / (us * 1e-6) / 1e12
+            fl = 4.0 * ao.nnz * wo.d * wo.B * wo.H
+            tf = fl / (us * 1e-6) / 1e12
+            mb = 4 * wo.B * wo.H * wo.L * wo.d * Qo.element_size()   # Q, K, V in, O out
+            gbs = mb / (us * 1e-6) / 1e9
+            peak = PEAK_BF16_TFLOPS if wo.dtype == "bf16" else PEAK_F32_TFLOPS
+            ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+            tr = load_traffic(wo.name).get("fused")
             others.append({"workload": wo.name, "dtype": wo.dtype, "us_per_call": round(us, 2),
                            "TFLOPs": round(tf, 2),
                            "pct_of_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)
                            if wo.dtype == "bf16" else None,
                            "kernel": f"k_fused_mfma<{wo.d}, bf16>" if wo.dtype == "bf16"
-                           else "k_fused_rows"})
+                           else "k_fused_rows",
+                           "roofline": {
+                               "bound": "mfma" if fl / mb > ridge else "hbm",
+                               "mfma": {"achieved": round(tf, 2), "peak": peak, "unit": "TFLOP/s",
+                                        "frac": round(tf / peak, 4)},
+                               "hbm": {"achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                                       "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                                       "min_bytes": mb,
+                                       "floor_us": round(mb / (PEAK_HBM_GBS * 1e9) * 1e6, 2)},
+                               "traffic": tr,
+                               "traffic_over_min": round(tr / mb, 3) if tr else None}})
             ao.close()
             del Qo, Ko, Vo, Oo
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, Q, K, V, args.cpu_seconds)
+        cpu = cpu_baseline(w, Q, K, V, args.cpu_seconds, O_gpu=O)
 
     line = {
         "metric": "sparse-MHSA fwd effective TFLOP/s on nnz (% of bf16 MFMA peak), L=4096",
@@ -324,6 +384,7 @@ def main() -> int:
         "unfused": unfused,
         "other_workloads": others,
         "cpu_baseline": cpu,
+        "max_abs_err": cpu["accuracy"]["max_abs_err"] if cpu and cpu.get("accuracy") else None,
     }
     print(json.dumps(line), flush=True)
     return 0

@@ -28,3 +28,24 @@ def gpu_lib():
     import paper_2407_16847_amd as splat
     splat.load()  # raises if libsplat.so is not built
     return splat
+
+
+# largest parity errors per workload, printed at the end of the run (also
+# under -q) so that every GPU run reports the margins it passed with
+_ERRORS = {}
+
+
+@pytest.fixture(scope="session")
+def record_errors():
+    def record(name, values):
+        _ERRORS[name] = dict(values)
+    return record
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    if not _ERRORS:
+        return
+    terminalreporter.section("largest errors against the oracle")
+    for name in sorted(_ERRORS):
+        terminalreporter.write_line(
+            f"{name}: " + ", ".join(f"{k} {v:.3e}" for k, v in _ERRORS[name].items()))

@@ -89,7 +89,7 @@ def _s_err_csr(x, ref, q, k, row_ptr, col_idx, scale):
 
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_small_configs_full_oracle(gpu_lib, cfg):
+def test_small_configs_full_oracle(gpu_lib, record_errors, cfg):
     splat = gpu_lib
     w = workloads.get(cfg)
     print(f"[gpu] cfg{cfg} {w.name} full-size dense oracle", flush=True)
@@ -118,6 +118,7 @@ def test_small_configs_full_oracle(gpu_lib, cfg):
             err = _s_err_csr(S[b, h], Sref[b, h], q[b, h], k[b, h], rp, ci, w.scale)
             assert err <= S_REL, f"S rel {err}"
     print(f"[gpu] cfg{cfg} errors {errs}", flush=True)
+    record_errors(f"cfg{cfg} {w.name}", errs)
 
 
 def _sample_rows(L, extra, rng, n_random=40):
@@ -138,7 +139,7 @@ def _s_err_dense(s_csr, ref_csr, q, k, mask, scale):
 
 
 @pytest.mark.parametrize("cfg", [4, 5])
-def test_large_configs_every_row(gpu_lib, cfg):
+def test_large_configs_every_row(gpu_lib, record_errors, cfg):
     """Full size, the benchmark's launch (bf16 in; fp32 and bf16 out): every
     row of every head of the fused and the unfused output against the dense
     fp64 oracle, and S and P element by element on four whole heads."""
@@ -184,6 +185,7 @@ def test_large_configs_every_row(gpu_lib, cfg):
             del Sd, Pd
     print(f"[gpu] cfg{cfg} max errors over all {w.B * w.H} heads: "
           + ", ".join(f"{k} {v:.3e}" for k, v in worst.items()), flush=True)
+    record_errors(f"cfg{cfg} {w.name} (all {w.B * w.H} heads)", worst)
 
 
 # --------------------------------------------------------------------------
