@@ -365,6 +365,32 @@ splat_status splat_sparse_mhsa_unfused(splat_acsr_t h, splat_dtype dtype, int32_
                                        void* stream);
 
 /*
+ * splat_sparse_mhsa_unfused_noalloc -- splat_sparse_mhsa_unfused for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): the same chain, the same
+ * kernels and the same results, with S (and, on the column-major branch,
+ * Pt) held in a scratch array inside the library instead of caller
+ * workspaces.  The caller passes Q, K, V and O as for
+ * splat_sparse_mhsa_unfused; the call allocates nothing.
+ *
+ * The scratch is a fixed SPLAT_NOALLOC_SCRATCH_BYTES (64 MiB) per device,
+ * held by every GPU the library runs on until the process ends.  A call needs
+ * B*H*nnz*4 bytes (rounded up to 256), plus B*H*nnz*4 more on the
+ * column-major branch; a larger request returns SPLAT_ERR_UNSUPPORTED before
+ * anything is enqueued.  The scratch is shared by every call on one device
+ * and keeps the last call's contents (every value it needs is rewritten
+ * first): calls that overlap on one device -- on different streams, or from
+ * several host threads without ordering -- race, so a caller serialises them
+ * (one stream does).  Other errors as splat_sparse_mhsa_unfused.
+ */
+#define SPLAT_NOALLOC_SCRATCH_BYTES (64u << 20)
+splat_status splat_sparse_mhsa_unfused_noalloc(splat_acsr_t h, splat_dtype dtype, int32_t B,
+                                               int32_t H, int32_t d, const void* Q, const void* K,
+                                               const void* V, float scale, void* O,
+                                               splat_dtype out_dtype, float alpha,
+                                               int32_t* used_colmajor, void* stream);
+
+/*
  * splat_sparse_mhsa_fwd -- the three steps fused: O = softmax_nz(scale * M (x) Q K^T) V
  * with an online (running max / running sum) softmax over the planned key
  * tiles, so S and P never reach device memory.  Q, K, V: [B,H,L,d] of `dtype`;

@@ -110,6 +110,8 @@ def load() -> ctypes.CDLL:
         "splat_row_softmax": [vp, i32, i32, vp, vp, vp],
         "splat_rspmm": [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp],
         "splat_sparse_mhsa_fwd": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, i32, vp],
+        "splat_sparse_mhsa_unfused_noalloc": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, i32, f32,
+                                              P(i32), vp],
         "splat_acsr_export_csc": [vp, vp, vp],
         "splat_acsr_tiling": [vp, i32, i32, i32, i32, P(TilingStats), vp, i64],
         "splat_transpose_colmajor": [vp, i32, i32, vp, vp, vp],
@@ -516,5 +518,35 @@ def sparse_mhsa_unfused(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, V: torch.T
     _check(load().splat_sparse_mhsa_unfused(
         acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(), V.data_ptr(), float(scale),
         S.data_ptr() if S.numel() else None, Pt.data_ptr() if Pt is not None and Pt.numel() else None,
+        O.data_ptr(), _DT[O.dtype], float(alpha), ctypes.byref(used), _stream()))
+    return O, bool(used.value)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20   # SPLAT_NOALLOC_SCRATCH_BYTES
+
+
+def sparse_mhsa_unfused_noalloc(acsr: Acsr, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                                scale: float, alpha: float = DENSE_ALPHA,
+                                O: Optional[torch.Tensor] = None,
+                                out_dtype: Optional[torch.dtype] = None):
+    """The unfused chain with S (and Pt) in the library's fixed scratch
+    instead of caller workspaces; returns (O, used_colmajor).  The call itself
+    allocates nothing (an O passed in is used as it is)."""
+    _dense(Q, "Q", acsr)
+    B, H, L, d = Q.shape
+    for n, x in (("K", K), ("V", V)):
+        _dense(x, n, acsr, d)
+        if x.dtype != Q.dtype or x.shape[:2] != Q.shape[:2]:
+            raise ValueError(f"{n} must match Q in dtype, B and H")
+        _on(x, n, Q)
+    odt = _out_dtype(out_dtype if O is None else O.dtype, Q.dtype)
+    if O is None:
+        O = torch.empty((B, H, L, d), dtype=odt, device=Q.device)
+    else:
+        _dense(O, "O", acsr, d)
+        _on(O, "O", Q, (B, H, L, d))
+    used = ctypes.c_int32(-1)
+    _check(load().splat_sparse_mhsa_unfused_noalloc(
+        acsr.handle, _DT[Q.dtype], B, H, d, Q.data_ptr(), K.data_ptr(), V.data_ptr(), float(scale),
         O.data_ptr(), _DT[O.dtype], float(alpha), ctypes.byref(used), _stream()))
     return O, bool(used.value)

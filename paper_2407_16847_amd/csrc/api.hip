@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cstdarg>
+#include <mutex>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -244,6 +245,43 @@ splat_status check_transpose(splat_acsr_t h, int32_t B, int32_t H, const float* 
     return fail(SPLAT_ERR_INVALID_ARG, "P and Pt must not overlap");
   CHECK(check_tile_grid(h, B, H));
   return SPLAT_OK;
+}
+
+// The paper's density analysis (section 9): masks at or above the density
+// alpha whose columns are single affine runs take the column-major layout.
+bool use_colmajor(const HostAcsr& a, float alpha) {
+  const double density = (double)a.nnz / ((double)a.L * (double)a.L);
+  return a.col_regular == 1 && a.nnz > 0 && density >= (double)alpha;
+}
+
+// Scratch of splat_sparse_mhsa_unfused_noalloc: the S values and, on the
+// column-major branch, their transposed copy.  Every GPU the library runs on
+// holds its own copy for the life of the process.  In host code `scratch`
+// names a host-side stand-in, never the device array: its device address is
+// looked up once per device (scratch_on) and only that address is used.
+constexpr size_t kScratchBytes = size_t(SPLAT_NOALLOC_SCRATCH_BYTES);
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+char* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// The scratch array's address on device `dev`, which is the current device.
+splat_status scratch_on(int dev, char** out) {
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(SPLAT_ERR_UNSUPPORTED, "the allocation-free call supports device ordinals below %d",
+                kMaxDevices);
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? (char*)p : nullptr;
+  });
+  if (g_scratch_err[dev] != hipSuccess || !g_scratch_ptr[dev])
+    return fail(SPLAT_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                hipGetErrorString(g_scratch_err[dev]));
+  *out = g_scratch_ptr[dev];
+  return ok();
 }
 
 }  // namespace
@@ -517,8 +555,7 @@ splat_status splat_sparse_mhsa_unfused(splat_acsr_t h, splat_dtype dtype, int32_
   CHECK(check_handle(h, B, H));
   const HostAcsr& a = h->host;
   // the paper's density analysis: dense masks take the column-major layout
-  const double density = (double)a.nnz / ((double)a.L * (double)a.L);
-  const bool col = a.col_regular == 1 && a.nnz > 0 && density >= (double)alpha;
+  const bool col = use_colmajor(a, alpha);
   // every step is validated before anything is enqueued
   CHECK(check_dtype(dtype, "dtype"));
   CHECK(check_d(d));
@@ -536,6 +573,29 @@ splat_status splat_sparse_mhsa_unfused(splat_acsr_t h, splat_dtype dtype, int32_
   }
   if (used_colmajor) *used_colmajor = col ? 1 : 0;
   return launch_rspmm(h, dtype, B, H, d, col ? Pt : S, V, O, out_dtype, col, st);
+}
+
+splat_status splat_sparse_mhsa_unfused_noalloc(splat_acsr_t h, splat_dtype dtype, int32_t B,
+                                               int32_t H, int32_t d, const void* Q, const void* K,
+                                               const void* V, float scale, void* O,
+                                               splat_dtype out_dtype, float alpha,
+                                               int32_t* used_colmajor, void* stream) {
+  CHECK(check_handle(h, B, H));
+  const HostAcsr& a = h->host;
+  const bool col = use_colmajor(a, alpha);
+  const size_t vals = (size_t)B * H * (size_t)a.nnz * sizeof(float);
+  const size_t s_bytes = (vals + 255) & ~size_t(255);
+  const size_t need = s_bytes + (col ? vals : 0);
+  if (need > kScratchBytes)
+    return fail(SPLAT_ERR_UNSUPPORTED,
+                "the allocation-free call needs %zu bytes of scratch (B*H*nnz*4%s), more than its "
+                "maximum of %zu bytes",
+                need, col ? ", twice for the column-major layout" : "", kScratchBytes);
+  char* base = nullptr;
+  CHECK(scratch_on(h->device, &base));
+  return splat_sparse_mhsa_unfused(h, dtype, B, H, d, Q, K, V, scale, (float*)base,
+                                   col ? (float*)(base + s_bytes) : nullptr, O, out_dtype, alpha,
+                                   used_colmajor, stream);
 }
 
 }  // extern "C"
