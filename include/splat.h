@@ -403,6 +403,33 @@ splat_status splat_sparse_mhsa_fwd(splat_acsr_t h, splat_dtype dtype, int32_t B,
                                    const void* Q, const void* K, const void* V, float scale,
                                    void* O, splat_dtype out_dtype, void* stream);
 
+/*
+ * splat_debug_bounds -- index checks of a checked build (built with
+ * -DSPLAT_DEBUG_BOUNDS: libsplat_checked.so beside libsplat.so; a debugging
+ * aid, not part of the method).  In a checked build every kernel checks the
+ * global-memory indices it derives from the plan and the ACSR runs -- query
+ * rows (bit 0), key rows of K and V (bit 1), positions in S and P (bit 2),
+ * positions in the column-major values (bit 3) -- against the sizes they
+ * index; an index outside is recorded and replaced by 0, so the access stays
+ * inside its buffer (the result is then wrong).  This call waits for the
+ * current device (hipDeviceSynchronize), sets *flags to the bits recorded on
+ * it since the last clear and, when `clear` is non-zero, clears them.
+ * Returns SPLAT_ERR_UNSUPPORTED in the regular build, SPLAT_ERR_INVALID_ARG
+ * for a NULL flags, SPLAT_ERR_HIP when the device reports an error.
+ */
+splat_status splat_debug_bounds(uint32_t* flags, int32_t clear);
+
+/*
+ * splat_debug_bounds_probe -- the checked build's test of its own mechanism:
+ * runs one index check on the current device, `index` against [0, n) as
+ * kind `kind` (0..3, the bits above), and sets *result to the checked index
+ * (index, or 0 when outside, with the kind's bit then recorded for
+ * splat_debug_bounds).  Allocates and frees one int of device memory and
+ * synchronises.  SPLAT_ERR_UNSUPPORTED in the regular build,
+ * SPLAT_ERR_INVALID_ARG for a NULL result or a kind outside 0..3.
+ */
+splat_status splat_debug_bounds_probe(int32_t kind, int32_t index, int32_t n, int32_t* result);
+
 /* Message of the calling thread's last non-OK status ("" if none). */
 const char* splat_last_error(void);
 

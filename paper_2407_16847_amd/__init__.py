@@ -73,18 +73,34 @@ class TilingStats(ctypes.Structure):
 TILING_METHODS = {"poset": 0, "grid": 1, "naive": 2}
 
 _LIB: Optional[ctypes.CDLL] = None
+_LIB_CHECKED: Optional[ctypes.CDLL] = None
 
 
-def lib_path() -> str:
-    return os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsplat.so")
+def lib_path(checked: bool = False) -> str:
+    name = "libsplat_checked.so" if checked else "libsplat.so"
+    return os.path.join(os.path.dirname(os.path.abspath(__file__)), name)
 
 
 def load() -> ctypes.CDLL:
     """Load libsplat.so (built in-tree).  Raises if it is missing."""
     global _LIB
-    if _LIB is not None:
-        return _LIB
-    path = lib_path()
+    if _LIB is None:
+        _LIB = _open(lib_path())
+    return _LIB
+
+
+def load_checked() -> ctypes.CDLL:
+    """Load libsplat_checked.so, the build with device-side index checks (a
+    debugging aid: the same C ABI, its kernels checking every index they derive
+    from the plan; see splat_debug_bounds).  The module's own calls keep using
+    libsplat.so; the checked library is driven through its C ABI directly."""
+    global _LIB_CHECKED
+    if _LIB_CHECKED is None:
+        _LIB_CHECKED = _open(lib_path(checked=True))
+    return _LIB_CHECKED
+
+
+def _open(path: str) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built; run `python -m paper_2407_16847_amd.build` "
                            "(or __graft_entry__.build()) first")
@@ -118,6 +134,8 @@ def load() -> ctypes.CDLL:
         "splat_rspmm_colmajor": [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp],
         "splat_sparse_mhsa_unfused": [vp, i32, i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, i32, f32,
                                       P(i32), vp],
+        "splat_debug_bounds": [P(ctypes.c_uint32), i32],
+        "splat_debug_bounds_probe": [i32, i32, i32, P(i32)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -127,7 +145,6 @@ def load() -> ctypes.CDLL:
     lib.splat_acsr_destroy.restype = None
     lib.splat_last_error.restype = ctypes.c_char_p
     lib.splat_version.restype = ctypes.c_char_p
-    _LIB = lib
     return lib
 
 

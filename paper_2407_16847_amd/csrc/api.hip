@@ -598,4 +598,38 @@ splat_status splat_sparse_mhsa_unfused_noalloc(splat_acsr_t h, splat_dtype dtype
                                    used_colmajor, stream);
 }
 
+splat_status splat_debug_bounds(uint32_t* flags, int32_t clear) {
+  CHECK(check_ptr(flags, "flags"));
+#ifndef SPLAT_DEBUG_BOUNDS
+  return fail(SPLAT_ERR_UNSUPPORTED,
+              "this library was built without SPLAT_DEBUG_BOUNDS (libsplat_checked.so has it)");
+#else
+  uint32_t bits = 0;
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = splat::bounds_collect_rows(&bits, clear != 0);
+  if (e == hipSuccess) e = splat::bounds_collect_mfma(&bits, clear != 0);
+  if (e == hipSuccess) e = splat::bounds_collect_tiles(&bits, clear != 0);
+  if (e != hipSuccess) return fail(SPLAT_ERR_HIP, "splat_debug_bounds: %s", hipGetErrorString(e));
+  *flags = bits;
+  return SPLAT_OK;
+#endif
+}
+
+splat_status splat_debug_bounds_probe(int32_t kind, int32_t index, int32_t n, int32_t* result) {
+  CHECK(check_ptr(result, "result"));
+  if (kind < 0 || kind > 3) return fail(SPLAT_ERR_INVALID_ARG, "kind %d is not 0..3", kind);
+#ifndef SPLAT_DEBUG_BOUNDS
+  (void)index;
+  (void)n;
+  return fail(SPLAT_ERR_UNSUPPORTED,
+              "this library was built without SPLAT_DEBUG_BOUNDS (libsplat_checked.so has it)");
+#else
+  int r = 0;
+  const hipError_t e = splat::bounds_probe(kind, index, n, &r);
+  if (e != hipSuccess) return fail(SPLAT_ERR_HIP, "splat_debug_bounds_probe: %s", hipGetErrorString(e));
+  *result = r;
+  return SPLAT_OK;
+#endif
+}
+
 }  // extern "C"

@@ -37,6 +37,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include "bounds.hpp"
 #include "launch.hpp"
 #include "mfma_util.hpp"
 
@@ -73,8 +74,8 @@ struct Geo {
 // exclude).  The 16 lanes of the mask load bring the wavefront's 32 row masks.
 template <int D>
 __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf16* Kh,
-                                           const __bf16* Vh, const uint64_t* masks, int wave,
-                                           int lane) {
+                                           const __bf16* Vh, const uint64_t* masks, int L,
+                                           int wave, int lane) {
   using G = Geo<D>;
   const int last = tl.nk - 1;
   // uniform tile bases (scalar registers) + 32-bit per-lane byte offsets
@@ -87,7 +88,8 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
     const int pos = lane % G::CPR;
     // one 32-bit lane offset from the scalar base: the load adds them itself
     // (no 64-bit vector address arithmetic)
-    const unsigned row = (unsigned)(tl.ks * min(r, last)) * (2u * D);
+    const int key = dbg::idx(tl.kb + tl.ks * min(r, last), L, dbg::kKey);
+    const unsigned row = (unsigned)(key - tl.kb) * (2u * D);
     const unsigned ko = row + 16u * (pos ^ swz_k(r)), vo = row + 16u * (pos ^ swz_v(r));
     dma16(kbase + ko, slot + bk * kDmaBlock);
     dma16(vbase + vo, slot + G::TB + bk * kDmaBlock);
@@ -195,7 +197,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
   const int qi = lane & 31, h = lane >> 5;
   const int m = wave * 32 + qi;
   const bool row_valid = m < grp.nrows;
-  const int row = row_valid ? rows[grp.row_off + m] : 0;
+  const int row = row_valid ? dbg::idx(rows[grp.row_off + m], L, dbg::kRow) : 0;
   const size_t head = (size_t)bh * L * D;
   const __bf16* Kh = K + head;
   const __bf16* Vh = V + head;
@@ -244,7 +246,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
     // prologue: the first NSLOT-1 tiles
 #pragma unroll
     for (int sl = 0; sl < NSLOT - 1; ++sl)
-      issue_tile<D>(smem + sl * G::SLOT, tiles[tb + min(sl, nt - 1)], Kh, Vh, masks, wave, lane);
+      issue_tile<D>(smem + sl * G::SLOT, tiles[tb + min(sl, nt - 1)], Kh, Vh, masks, L, wave,
+                    lane);
     // descriptors are read one iteration before they are needed
     Tile next_issue = tiles[tb + min(NSLOT - 1, nt - 1)];
     int next_flags = tiles[tb].flags;
@@ -256,7 +259,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
       const int flags = next_flags;
       next_issue = tiles[tb + min(i + NSLOT, nt - 1)];
       next_flags = tiles[tb + min(i + 1, nt - 1)].flags;
-      issue_tile<D>(smem + ((i + NSLOT - 1) % NSLOT) * G::SLOT, to_issue, Kh, Vh, masks, wave,
+      issue_tile<D>(smem + ((i + NSLOT - 1) % NSLOT) * G::SLOT, to_issue, Kh, Vh, masks, L, wave,
                     lane);
       const int wst = (flags >> (kWaveShift + 2 * wave)) & 3;
       if (wst != kWaveEmpty) {
@@ -387,6 +390,8 @@ hipError_t fused_d(const DevAcsr& a, int BH, const void* Q, const void* K, const
 }
 
 }  // namespace
+
+hipError_t bounds_collect_mfma(uint32_t* bits, bool clear) { return dbg::collect(bits, clear); }
 
 hipError_t prepare_fused_mfma() {
   hipError_t e = allow_lds<64, float>();

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include "bounds.hpp"
 #include "launch.hpp"
 
 namespace splat {
@@ -66,12 +67,14 @@ __global__ __launch_bounds__(kWave) void k_rsddmm_rows(DevAcsr a, int d, const T
   __syncthreads();
   const RowRuns rr = a.runs[i];
   float* out = S + (size_t)bh * a.nnz + a.row_ptr[i];
+  const int64_t r0 = a.row_ptr[i];   // out's position in the head
 #pragma unroll
   for (int r = 0; r < SPLAT_MAX_RUNS; ++r) {
     const Run q = rr.r[r];
     for (int k = lane; k < q.count; k += kWave) {
-      const int j = q.start + q.stride * k;
-      out[q.prefix + k] = dot_row(qs, K + head + (size_t)j * d, d) * scale;
+      const int j = dbg::idx(q.start + q.stride * k, a.L, dbg::kKey);
+      out[dbg::rel(q.prefix + k, r0, a.nnz, dbg::kValue)] =
+          dot_row(qs, K + head + (size_t)j * d, d) * scale;
     }
   }
 }
@@ -85,6 +88,7 @@ __global__ __launch_bounds__(kWave) void k_rspmm_rows(DevAcsr a, int d, const fl
   const int i = blockIdx.x, bh = blockIdx.y, lane = threadIdx.x;
   const size_t head = (size_t)bh * a.L * d;
   const float* p = P + (size_t)bh * a.nnz + (COL ? 0 : a.row_ptr[i]);
+  const int64_t r0 = COL ? 0 : a.row_ptr[i];   // p's position in the head
   const RowRuns rr = a.runs[i];
   const bool two = d > kWave;
   float acc0 = 0.f, acc1 = 0.f;
@@ -93,8 +97,9 @@ __global__ __launch_bounds__(kWave) void k_rspmm_rows(DevAcsr a, int d, const fl
     const Run q = rr.r[r];
 #pragma unroll 4
     for (int k = 0; k < q.count; ++k) {
-      const int j = q.start + q.stride * k;
-      const float pk = COL ? p[col_pos(a.cols[j], i)] : p[q.prefix + k];
+      const int j = dbg::idx(q.start + q.stride * k, a.L, dbg::kKey);
+      const float pk = COL ? p[dbg::idx((int64_t)col_pos(a.cols[j], i), a.nnz, dbg::kColPos)]
+                           : p[dbg::rel(q.prefix + k, r0, a.nnz, dbg::kValue)];
       const T* v = V + head + (size_t)j * d;
       acc0 = fmaf(pk, to_f32(v[lane]), acc0);
       if (two) acc1 = fmaf(pk, to_f32(v[lane + kWave]), acc1);
@@ -129,7 +134,7 @@ __global__ __launch_bounds__(kWave) void k_fused_rows(DevAcsr a, int d, const T*
     int j = 0;
     float s = -INFINITY;
     if (valid) {
-      j = col_of(rr, k);
+      j = dbg::idx(col_of(rr, k), a.L, dbg::kKey);
       s = dot_row(qs, K + head + (size_t)j * d, d) * scale;
     }
     const float mn = fmaxf(m, wave_max(s));      // finite: lane 0 is valid
@@ -157,7 +162,36 @@ __global__ __launch_bounds__(kWave) void k_fused_rows(DevAcsr a, int d, const T*
   if (two) store(o + lane + kWave, acc1 * inv);
 }
 
+#ifdef SPLAT_DEBUG_BOUNDS
+// One index check on the device (the checked build's own test): out = the
+// checked index.
+__global__ void k_bounds_probe(int kind, int index, int n, int* out) {
+  *out = dbg::idx(index, n, (dbg::Kind)kind);
+}
+#endif
+
 }  // namespace
+
+hipError_t bounds_collect_rows(uint32_t* bits, bool clear) { return dbg::collect(bits, clear); }
+
+hipError_t bounds_probe(int kind, int index, int n, int* result) {
+#ifndef SPLAT_DEBUG_BOUNDS
+  (void)kind;
+  (void)index;
+  (void)n;
+  (void)result;
+  return hipErrorNotSupported;
+#else
+  int* d = nullptr;
+  hipError_t e = hipMalloc(&d, sizeof(int));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_bounds_probe, dim3(1), dim3(1), 0, 0, kind, index, n, d);
+  e = hipGetLastError();
+  if (e == hipSuccess) e = hipMemcpy(result, d, sizeof(int), hipMemcpyDeviceToHost);
+  const hipError_t f = hipFree(d);
+  return e != hipSuccess ? e : f;
+#endif
+}
 
 hipError_t launch_rsddmm_rows(const DevAcsr& a, int dtype, int BH, int d, const void* Q,
                               const void* K, float scale, float* S, hipStream_t st) {

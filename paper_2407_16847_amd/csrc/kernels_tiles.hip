@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include "bounds.hpp"
 #include "launch.hpp"
 #include "mfma_util.hpp"
 
@@ -84,7 +85,7 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
   const int qi = lane & 31, h = lane >> 5;
   const int m = wave * kWaveRows + qi;
   const bool row_valid = m < grp.nrows;
-  const int row = row_valid ? rows[grp.row_off + m] : 0;
+  const int row = row_valid ? dbg::idx(rows[grp.row_off + m], L, dbg::kRow) : 0;
   const size_t head = (size_t)bh * L * D;
   const __bf16* Kh = K + head;
 
@@ -107,6 +108,7 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
   // (S is 16-byte aligned): the row's values sit at [lead, lead + row_len)
   // from its line base S + rline.
   const int64_t sidx = row_valid ? (int64_t)bh * nnz + row_ptr[row] : 0;
+  const int64_t total = (int64_t)BH * nnz;   // values of S over all heads
   const int lead = (int)((((uintptr_t)S >> 2) + (uint64_t)sidx) & 31u);
   const int64_t rline = sidx - lead;
   const int row_len = row_valid ? row_ptr[row + 1] - row_ptr[row] : 0;
@@ -125,7 +127,8 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
     const int last = tl.nk - 1;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2) {
-      const __bf16* krow = Kh + (size_t)(tl.kb + tl.ks * min(32 * kb2 + qi, last)) * D + 8 * h;
+      const int key = dbg::idx(tl.kb + tl.ks * min(32 * kb2 + qi, last), L, dbg::kKey);
+      const __bf16* krow = Kh + (size_t)key * D + 8 * h;
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) ka[kb2][ks] = *(const bf16x8_t*)(krow + 16 * ks);
     }
@@ -184,13 +187,15 @@ __global__ __launch_bounds__(kTileThreads, D == 64 ? 3 : 2) void k_rsddmm_tiles(
         if (a >= hi) continue;
         if (a >= lo && a + 4 <= hi) {
           const f32x4u_t v = *(const f32x4u_t*)(srow + a);
-          __builtin_nontemporal_store(v, (f32x4u_t*)(grow + a));
+          __builtin_nontemporal_store(v, (f32x4u_t*)(grow + dbg::rel(a, rl[it], total - 3,
+                                                                     dbg::kValue)));
         } else {
           // the row's first or last line: single values, cached so that the
           // rest of the line (the neighbouring row's) merges with them
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (a + e >= lo && a + e < hi) grow[a + e] = srow[a + e];
+            if (a + e >= lo && a + e < hi)
+              grow[dbg::rel(a + e, rl[it], total, dbg::kValue)] = srow[a + e];
         }
       }
       // what is left of the row, [hi, en), moves to just before kCarry
@@ -282,6 +287,7 @@ __global__ __launch_bounds__(256) void k_softmax_seg(const int32_t* __restrict__
     const int32_t b0 = row_ptr[i];
     n = row_ptr[i + 1] - b0;
     base = (size_t)bh * nnz + b0;
+    if (!dbg::check(n == 0 || (b0 >= 0 && b0 + (int64_t)n <= nnz), dbg::kValue)) n = 0;
   }
   // every lane takes part in the segment reductions; lanes without a row see n = 0
   float x[4];
@@ -315,6 +321,7 @@ __global__ __launch_bounds__(256) void k_softmax(const int32_t* __restrict__ row
   const int32_t b0 = row_ptr[i];
   const int n = row_ptr[i + 1] - b0;
   if (n == 0) return;
+  if (!dbg::check(b0 >= 0 && b0 + (int64_t)n <= nnz, dbg::kValue)) return;
   const size_t base = (size_t)bh * nnz + b0;
   const float* s = S + base;
   float* p = P + base;
@@ -407,7 +414,7 @@ __global__ __launch_bounds__(kTileThreads, (COL && D == 128) ? 1 : 2) void k_rsp
   const int qi = lane & 31, h = lane >> 5;
   const int m = wave * kWaveRows + qi;
   const bool row_valid = m < grp.nrows;
-  const int row = row_valid ? rows[grp.row_off + m] : 0;
+  const int row = row_valid ? dbg::idx(rows[grp.row_off + m], L, dbg::kRow) : 0;
   const size_t head = (size_t)bh * L * D;
   const __bf16* Vh = V + head;
   const float* prow = P + (size_t)bh * nnz + (COL ? 0 : row_ptr[row]);
@@ -426,7 +433,8 @@ __global__ __launch_bounds__(kTileThreads, (COL && D == 128) ? 1 : 2) void k_rsp
     for (int k = 0; k < CPT; ++k) {
       const int idx = tid + kTileThreads * k;
       const int r = idx / CPR, c = idx % CPR;
-      reg[k] = *(const u32x4_t*)(Vh + (size_t)(tl.kb + tl.ks * min(r, tl.nk - 1)) * D + 8 * c);
+      const int key = dbg::idx(tl.kb + tl.ks * min(r, tl.nk - 1), L, dbg::kKey);
+      reg[k] = *(const u32x4_t*)(Vh + (size_t)key * D + 8 * c);
     }
   };
   auto store_v = [&](char* slot, const u32x4_t (&reg)[CPT]) {
@@ -476,15 +484,20 @@ __global__ __launch_bounds__(kTileThreads, (COL && D == 128) ? 1 : 2) void k_rsp
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
               const int u = 16 * j + 8 * (e >> 2) + 4 * h + (e & 3);
-              pv[j][e] = ((bits >> u) & 1ull) ? prow[col_pos(cc[u], row)] : 0.f;
+              pv[j][e] = ((bits >> u) & 1ull)
+                             ? prow[dbg::idx((int64_t)col_pos(cc[u], row), nnz, dbg::kColPos)]
+                             : 0.f;
             }
         } else if (row_valid) {
           const float* src = prow + cnt;
+          const int64_t rpos = (int64_t)row_ptr[row] + cnt;   // src's position in the head
           if (wst == kWaveFull) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-              const f32x4u_t a = *(const f32x4u_t*)(src + 16 * j + 4 * h);
-              const f32x4u_t b = *(const f32x4u_t*)(src + 16 * j + 8 + 4 * h);
+              const f32x4u_t a =
+                  *(const f32x4u_t*)(src + dbg::rel(16 * j + 4 * h, rpos, nnz - 3, dbg::kValue));
+              const f32x4u_t b = *(const f32x4u_t*)(src + dbg::rel(16 * j + 8 + 4 * h, rpos,
+                                                                     nnz - 3, dbg::kValue));
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 pv[j][e] = a[e];
@@ -494,7 +507,8 @@ __global__ __launch_bounds__(kTileThreads, (COL && D == 128) ? 1 : 2) void k_rsp
           } else {
             // key 8*g + 4*h + e is element 4*(g%2) + e of k-step g/2
             for_each_key(bits, h, [&](int g, int e, unsigned present, int pos) {
-              pv[g >> 1][4 * (g & 1) + e] = present ? src[pos] : 0.f;
+              pv[g >> 1][4 * (g & 1) + e] =
+                  present ? src[dbg::rel(pos, rpos, nnz, dbg::kValue)] : 0.f;
             });
           }
         } else {
@@ -577,22 +591,27 @@ __global__ __launch_bounds__(kTileThreads) void k_colmajor_tiles(
     if (row_valid && wst == kWaveFull) {
       // the row's 32 values for this half are contiguous: 16-byte loads
       const float* src = prow + cnt + 32 * h;
+      const int64_t rpos = (int64_t)row_ptr[row] + cnt + 32 * h;   // src's position in the head
       float v[32];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        const f32x4u_t x = *(const f32x4u_t*)(src + 4 * q);
+        const f32x4u_t x = *(const f32x4u_t*)(src + dbg::rel(4 * q, rpos, nnz - 3, dbg::kValue));
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[4 * q + e] = x[e];
       }
 #pragma unroll
-      for (int u = 0; u < 32; ++u) dst[col_pos(ct[32 * h + u], row)] = v[u];
+      for (int u = 0; u < 32; ++u)
+        dst[dbg::idx((int64_t)col_pos(ct[32 * h + u], row), nnz, dbg::kColPos)] = v[u];
     } else if (row_valid) {
       const unsigned hb = (unsigned)(bits >> (32 * h));
       const float* src = prow + cnt + (h ? __builtin_popcount((unsigned)bits) : 0);
+      const int64_t rpos =   // src's position in the head
+          (int64_t)row_ptr[row] + cnt + (h ? __builtin_popcount((unsigned)bits) : 0);
       int k = 0;
       for (int u = 0; u < 32; ++u) {
         if ((hb >> u) & 1u) {
-          dst[col_pos(ct[32 * h + u], row)] = src[k];
+          dst[dbg::idx((int64_t)col_pos(ct[32 * h + u], row), nnz, dbg::kColPos)] =
+              src[dbg::rel(k, rpos, nnz, dbg::kValue)];
           ++k;
         }
       }
@@ -600,6 +619,12 @@ __global__ __launch_bounds__(kTileThreads) void k_colmajor_tiles(
     cnt += popc64(bits);
   }
 }
+
+}  // namespace
+
+hipError_t bounds_collect_tiles(uint32_t* bits, bool clear) { return dbg::collect(bits, clear); }
+
+namespace {
 
 template <int NV>
 hipError_t softmax_launch(const DevAcsr& a, int BH, const float* S, float* P, hipStream_t st) {

@@ -62,6 +62,16 @@ hipError_t launch_softmax(const DevAcsr& a, int BH, const float* S, float* P, hi
 // the handle's device, so launches never change kernel attributes.
 hipError_t prepare_fused_mfma();
 
+// Index checks of a build with -DSPLAT_DEBUG_BOUNDS (no-ops otherwise): each
+// kernel file's flags on the current device, OR-ed into *bits (bit k = kind
+// k of bounds.hpp), cleared when `clear`.
+hipError_t bounds_collect_rows(uint32_t* bits, bool clear);
+hipError_t bounds_collect_mfma(uint32_t* bits, bool clear);
+hipError_t bounds_collect_tiles(uint32_t* bits, bool clear);
+// One check of `index` against [0, n) as kind `kind`, run on the device
+// (allocates and frees one int); *result = the checked index.
+hipError_t bounds_probe(int kind, int index, int n, int* result);
+
 hipError_t launch_fused_mfma(const DevAcsr& a, int BH, int d, const void* Q, const void* K,
                              const void* V, float scale, void* O, int out_dtype, hipStream_t st);
 

@@ -37,6 +37,24 @@ def test_library_exports_every_declared_symbol(lib):
     for n in names:
         assert hasattr(lib, n), n
     assert lib.splat_version().startswith(b"splat-mi355x")
+    checked = splat.load_checked()   # the build with device-side index checks
+    for n in names:
+        assert hasattr(checked, n), n
+
+
+def test_index_checks_only_in_the_checked_build(lib):
+    """splat_debug_bounds and its probe: unsupported in the regular build,
+    argument errors caught on the host in both (no device call is made)."""
+    flags, r = ctypes.c_uint32(7), ctypes.c_int32(7)
+    assert lib.splat_debug_bounds(ctypes.byref(flags), 1) == 2          # UNSUPPORTED
+    assert b"SPLAT_DEBUG_BOUNDS" in lib.splat_last_error()
+    assert lib.splat_debug_bounds_probe(1, 5, 3, ctypes.byref(r)) == 2
+    assert flags.value == 7 and r.value == 7                              # nothing written
+    for l in (lib, splat.load_checked()):
+        assert l.splat_debug_bounds(None, 0) == 1                         # INVALID_ARG
+        assert l.splat_debug_bounds_probe(0, 0, 1, None) == 1
+        assert l.splat_debug_bounds_probe(4, 0, 1, ctypes.byref(r)) == 1   # no such kind
+        assert l.splat_debug_bounds_probe(-1, 0, 1, ctypes.byref(r)) == 1
 
 
 def test_single_hip_runtime_in_process(lib):
