@@ -20,7 +20,7 @@
 //      or PARTIAL; on PARTIAL tiles the scores outside each row's affine
 //      runs are set to -inf from the row's precomputed 64-bit tile mask
 //   4. online softmax against a per-row integer reference m: p = exp2(t - m).
-//      The fast pass computes exp2(t), rounds it toward zero to bf16 and,
+//      The fast pass computes exp2(t), rounds it to nearest even bf16 and,
 //      only when some row has m > 0, applies 2^-m to each bf16 pair with one
 //      saturating 16-bit subtract from the exponent fields -- no per-score
 //      max, offset or multiply.  m stays 0 while a row's scores stay within
@@ -31,9 +31,11 @@
 //      reference lies outside [0, 100]
 //   5. O^T += V^T P^T on the same MFMA, P^T taken straight from the score
 //      registers, V^T gathered by LDS transpose reads in the key order the
-//      score registers imply; the row sum adds the same rounded p
+//      score registers imply; the row sum adds the same rounded p, so a row
+//      with one key returns that key's V row exactly
 //
-// At the end O = O^T / (row sum), written in the requested dtype.
+// At the end O = O^T / (row sum), written in the requested dtype through LDS
+// as whole rows (16-byte non-temporal stores along each row).
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -103,28 +105,33 @@ __device__ __forceinline__ void issue_tile(char* slot, const Tile tl, const __bf
   }
 }
 
-// Fast pass of one tile: p = exp2(t) * 2^-m for this lane's 32 scores t
-// (s * scale*log2(e), from the pre-scaled Q) and the row's integer reference
-// m >= 0.  exp2(t) is rounded toward zero to bf16 (one v_perm_b32 per pair)
-// and summed; returns that sum.  The factor 2^-m is applied afterwards, by
-// scale_pairs, only when some row of the wavefront has m > 0.
-__device__ __forceinline__ float tile_exp_fast(const f32x16_t* s, bf16x8_t* pf) {
+// One tile's exponentials for this lane's 32 scores t (s * scale*log2(e),
+// from the pre-scaled Q): p = exp2(t - m) with REF, else p = exp2(t) (the fast
+// pass, whose factor 2^-m is applied afterwards by scale_pairs, only when some
+// row of the wavefront has m > 0).  Each p goes to the P^T operand rounded to
+// nearest even bf16 (one v_cvt_pk_bf16_f32 per pair); returns the sum of the
+// rounded p (v_dot2c_f32_bf16 against ones, fp32 accumulation).
+template <bool REF>
+__device__ __forceinline__ float tile_exp(const f32x16_t* s, float m, bf16x8_t* pf) {
   float l0 = 0.f, l1 = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     float e8[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) e8[e] = exp2_hw(s[j >> 1][(j & 1) * 8 + e]);
-    bf16x2_t p2[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) p2[e] = pack_bf16_rz(e8[2 * e], e8[2 * e + 1]);
-    pf[j] = __builtin_shufflevector(__builtin_shufflevector(p2[0], p2[1], 0, 1, 2, 3),
-                                    __builtin_shufflevector(p2[2], p2[3], 0, 1, 2, 3), 0, 1, 2, 3,
-                                    4, 5, 6, 7);
-    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[0], kOnes2, l0, false);
-    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[1], kOnes2, l1, false);
-    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[2], kOnes2, l0, false);
-    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[3], kOnes2, l1, false);
+    for (int e = 0; e < 8; ++e) {
+      const float t = s[j >> 1][(j & 1) * 8 + e];
+      e8[e] = exp2_hw(REF ? t - m : t);
+    }
+    // the row sum adds exactly the rounded values the MFMA multiplies; the
+    // dot products take the packed pairs as scalars (taken back out of a
+    // vector, the compiler merged the two sums into one)
+    const unsigned u0 = pack_bf16_rn(e8[0], e8[1]), u1 = pack_bf16_rn(e8[2], e8[3]);
+    const unsigned u2 = pack_bf16_rn(e8[4], e8[5]), u3 = pack_bf16_rn(e8[6], e8[7]);
+    l0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0), kOnes2, l0, false);
+    l1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1), kOnes2, l1, false);
+    l0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u2), kOnes2, l0, false);
+    l1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u3), kOnes2, l1, false);
+    pf[j] = __builtin_bit_cast(bf16x8_t, u32x4_t{u0, u1, u2, u3});
   }
   return l0 + l1;
 }
@@ -141,28 +148,6 @@ __device__ __forceinline__ void scale_pairs(bf16x8_t* pf, unsigned msub) {
   for (int j = 0; j < 4; ++j)
     pf[j] = __builtin_bit_cast(bf16x8_t, __builtin_elementwise_sub_sat(
                                              __builtin_bit_cast(u16x8_t, pf[j]), sub));
-}
-
-// Slow pass: p = exp2(t - m) with the reference subtracted in fp32.
-__device__ __forceinline__ float tile_exp_ref(const f32x16_t* s, float m, bf16x8_t* pf) {
-  float l0 = 0.f, l1 = 0.f;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    float e8[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) e8[e] = exp2_hw(s[j >> 1][(j & 1) * 8 + e] - m);
-    bf16x2_t p2[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) p2[e] = pack_bf16_rz(e8[2 * e], e8[2 * e + 1]);
-    pf[j] = __builtin_shufflevector(__builtin_shufflevector(p2[0], p2[1], 0, 1, 2, 3),
-                                    __builtin_shufflevector(p2[2], p2[3], 0, 1, 2, 3), 0, 1, 2, 3,
-                                    4, 5, 6, 7);
-    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[0], kOnes2, l0, false);
-    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[1], kOnes2, l1, false);
-    l0 = __builtin_amdgcn_fdot2_f32_bf16(p2[2], kOnes2, l0, false);
-    l1 = __builtin_amdgcn_fdot2_f32_bf16(p2[3], kOnes2, l1, false);
-  }
-  return l0 + l1;
 }
 
 // scores outside the row's affine runs in this tile set to -inf
@@ -289,7 +274,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
           mask_scores(sacc, mk, h);
         }
         bf16x8_t pf[4];
-        float lt = tile_exp_fast(sacc, pf);
+        float lt = tile_exp<false>(sacc, 0.f, pf);
         if (__any(msub != 0u)) {
           scale_pairs(pf, msub);
           lt *= mscale;   // 2^-m: the sum of the scaled pairs, exactly
@@ -322,7 +307,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
           // a power of two, 1 if unchanged; a row with nothing accumulated
           // has nothing to rescale (and its reference may fall)
           const float alpha = acc ? exp2_hw(m_run - m_new) : 0.f;
-          lt = tile_exp_ref(sacc, m_new, pf);
+          lt = tile_exp<true>(sacc, m_new, pf);
           lrow = lt + lane_xor32(lt);
           l_run *= alpha;
           m_run = m_new;
@@ -353,16 +338,33 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void k_fused_mfma(
 
   const float l_tot = l_run + lane_xor32(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (row_valid) {
-    OutT* orow = O + head + (size_t)row * D;
+  // O leaves through LDS: each wavefront stages its 32 rows (rows padded by
+  // 16 bytes; after the loop's last barrier no wavefront reads the ring), then
+  // writes whole rows, 16 bytes per lane with consecutive lanes along a row,
+  // as non-temporal stores: no partial lines, and nothing left dirty in L2.
+  constexpr int SZ = (int)sizeof(OutT);
+  constexpr int RS = D * SZ + 16;      // staged row stride, bytes
+  constexpr int CPRO = D * SZ / 16;    // 16-byte chunks per output row
+  static_assert(4 * 32 * RS <= G::LDS, "output staging fits in the ring");
+  char* stage = smem + wave * 32 * RS;
 #pragma unroll
-    for (int b = 0; b < NDB; ++b)
+  for (int b = 0; b < NDB; ++b)
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int d0 = b * 32 + rg * 8 + 4 * h;
-        store4<OutT>(orow + d0, oacc[b][4 * rg] * inv, oacc[b][4 * rg + 1] * inv,
-                     oacc[b][4 * rg + 2] * inv, oacc[b][4 * rg + 3] * inv);
-      }
+    for (int rg = 0; rg < 4; ++rg) {
+      const int d0 = b * 32 + rg * 8 + 4 * h;
+      store4<OutT>((OutT*)(stage + qi * RS + d0 * SZ), oacc[b][4 * rg] * inv,
+                   oacc[b][4 * rg + 1] * inv, oacc[b][4 * rg + 2] * inv,
+                   oacc[b][4 * rg + 3] * inv);
+    }
+  const int nrows_w = grp.nrows - wave * 32;   // valid rows of this wavefront
+  char* ohead = (char*)(O + head);
+#pragma unroll
+  for (int k = 0; k < 32 * CPRO / 64; ++k) {
+    const int idx = k * 64 + lane;
+    const int r = idx / CPRO, c = idx % CPRO;
+    const int orow = __shfl(row, r);           // lane r holds query row r of the wavefront
+    const u32x4_t v = *(const u32x4_t*)(stage + r * RS + c * 16);
+    if (r < nrows_w) store16_nt(ohead + (size_t)orow * (D * SZ) + c * 16, v);
   }
 }
 

@@ -158,12 +158,16 @@ __device__ __forceinline__ void read_v_operands(unsigned vbase, const int (&voff
   lds_wait<D / 32>(va);
 }
 
-// Two fp32 values to a bf16 pair by dropping their low 16 bits (rounding
-// toward zero): one full-rate v_perm_b32 instead of a half-rate conversion.
-__device__ __forceinline__ bf16x2_t pack_bf16_rz(float lo, float hi) {
-  const unsigned r = __builtin_amdgcn_perm(__builtin_bit_cast(unsigned, hi),
-                                           __builtin_bit_cast(unsigned, lo), 0x07060302u);
-  return __builtin_bit_cast(bf16x2_t, r);
+// Two fp32 values to a bf16 pair, rounded to nearest even (one
+// v_cvt_pk_bf16_f32).
+__device__ __forceinline__ unsigned pack_bf16_rn(float lo, float hi) {
+  const bf16x2_t p = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(unsigned, p);
+}
+
+// 16-byte non-temporal store (streamed past the caches)
+__device__ __forceinline__ void store16_nt(void* p, u32x4_t v) {
+  __builtin_nontemporal_store(v, (u32x4_t*)p);
 }
 
 // x where bit u of `word` is set, -inf elsewhere (v_bfe_i32 + v_bfi_b32)
